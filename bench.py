@@ -1,0 +1,246 @@
+"""Benchmark of the FASGD parameter-server step on one MI355X.
+
+One step = the whole server path over one batch of client gradients:
+  1. fasgd_apply_updates  K gradients fused in one pass (dense FASGD,
+                          eqs. of Sec. 2.2, K-fold state reuse);
+  2. bfasgd_select_compact one more client's push, per-parameter send/skip
+                          (Sec. 2.3) and compaction into (index, value);
+  3. bfasgd_apply_sparse  the server applies that compacted push.
+Inputs (state and a pool of K + 1 distinct synthetic gradients) are resident
+in HBM before timing; every step uses fresh (client, timestamp) pairs.
+
+Prints ONE JSON line.  value = parameter updates applied per second
+(P*K dense + m sparse per step).  roofline = the dense apply kernel's
+algorithmic HBM bytes per launch over its average event-timed duration.
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "param-updates/sec and achieved HBM GB/s (% of peak), FASGD apply at 25M/1B params"
+HBM_PEAK_GBS = 8000.0
+EPS_C = 1e-8
+SEED = 0x5EED
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "fasgd_dense_k32_memscale_1e9_pmc.txt")
+DENSE_SOURCES = [os.path.join(ROOT, "paper_1601_04033_amd", "csrc", f) for f in ("dense.hip", "device_math.hpp")]
+
+
+def dense_source_hash():
+    h = hashlib.sha256()
+    for f in DENSE_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(P, K):
+    """HBM bytes per dense launch from the committed rocprofv3 counter
+    summary, or None when it is absent or the kernel changed since."""
+    if not os.path.exists(PMC_SUMMARY):
+        return None
+    text = open(PMC_SUMMARY).read()
+    m_hash = re.search(r"source_hash:\s*([0-9a-f]+)", text)
+    m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    m_shape = re.search(r"shape:\s*P=(\d+)\s+K=(\d+)", text)
+    if not (m_hash and m_bytes and m_shape) or m_hash.group(1) != dense_source_hash():
+        return None
+    if int(m_shape.group(1)) != P or int(m_shape.group(2)) != K:
+        return None
+    return float(m_bytes.group(1))
+
+
+def calibrate_c(v, target, n=1 << 20):
+    """Threshold c with mean_j t_j/(t_j + c) = target over a sample of v."""
+    import numpy as np
+    import torch
+    P = v.numel()
+    g = torch.Generator(device=v.device)
+    g.manual_seed(1)
+    sample = v[torch.randint(0, P, (min(n, P),), device=v.device, generator=g)]
+    t = sample.double().cpu().numpy() + EPS_C
+    lo, hi = 0.0, 1e9
+    for _ in range(200):
+        c = 0.5 * (lo + hi)
+        lo, hi = (c, hi) if (t / (t + c)).mean() > target else (lo, c)
+    return float(np.float32(c))
+
+
+def cpu_baseline(pool, theta0_host, clients, ts, c, w, K, P_s):
+    """The oracle (single-threaded C, fp64) on the first P_s parameters of the
+    same step: K dense updates, one selection, one sparse apply."""
+    import numpy as np
+    import oracle
+    grads = [g[:P_s].cpu().numpy() for g in pool]
+    st = oracle.init_state(theta0_host[:P_s], alpha=w.alpha_fasgd)
+    t0 = time.perf_counter()
+    for k in range(K):
+        oracle.fasgd_apply(st, grads[k], ts[k])
+    idx, val, m = oracle.bfasgd_select(st.v.astype(np.float32), grads[K], c, EPS_C, SEED, st.T, clients[K])
+    oracle.bfasgd_apply_sparse(st, idx, val, ts[K])
+    dt = time.perf_counter() - t0
+    return (P_s * K + m) / dt, dt, m
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="memscale", choices=["memscale", "large"])
+    ap.add_argument("--K", type=int, default=32)
+    ap.add_argument("--math", default="fast", choices=["fast", "ieee"])
+    ap.add_argument("--cpu-params", type=int, default=1 << 23,
+                    help="parameters in the oracle's CPU-baseline sample (0 = skip)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this build runs on one GPU: the server update is elementwise and "
+                                   "would shard by parameter range with no exchange, but no multi-GPU "
+                                   "path is built; run with --gpus 1"}), flush=True)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_1601_04033_amd as fa
+    import workload
+
+    fa.load_library()
+    dev = torch.device("cuda:0")
+    w = workload.WORKLOADS[args.workload]
+    P, K = w.P, args.K
+    f = w.transmit_fraction or 0.1
+    mode = fa.MATH_FAST if args.math == "fast" else fa.MATH_IEEE
+    steps, warm = args.steps, args.warmup
+
+    print(f"# setup: workload={args.workload} P={P} K={K} math={args.math}", file=sys.stderr, flush=True)
+    theta0, m, s = workload.device_params(w, dev)
+    theta0_host = theta0[: args.cpu_params].cpu().numpy() if args.cpu_params else None
+    pool = [workload.device_gradient(w, m, s, t) for t in range(K + 1)]
+    del m, s
+    theta, n, b, v, last_T = fa.allocate_state(P, dev)
+    theta.copy_(theta0)
+    del theta0
+    st = fa.fasgd_init_state(theta, n, b, v, last_T, lam=w.lam, alpha=w.alpha_fasgd, math_mode=mode)
+    cap = P
+    idx = torch.empty(cap, device=dev, dtype=torch.int32)
+    val = torch.empty(cap, device=dev)
+    cnt = torch.zeros(1, device=dev, dtype=torch.int64)
+    ws = fa.allocate_workspace(P, dev)
+    per_step = K + 1
+    clients, ts = workload.schedule(w, K + (warm + steps + 4) * per_step)
+    torch.cuda.synchronize()
+
+    ev = {name: [] for name in ("dense", "select", "sparse")}
+    counts = []
+
+    def step(timed, c):
+        base = st.T                          # the schedule is indexed by server timestamp
+        sl = slice(base, base + K)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e2 = torch.cuda.Event(enable_timing=True)
+        e3 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fa.fasgd_apply_updates(st, pool[:K], clients[sl], ts[sl])
+        e1.record()
+        fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, st.T, clients[base + K], idx, val, cnt, ws)
+        e2.record()
+        fa.bfasgd_apply_sparse(st, idx, val, cnt, clients[base + K], ts[base + K])
+        e3.record()
+        if timed:
+            ev["dense"].append((e0, e1))
+            ev["select"].append((e1, e2))
+            ev["sparse"].append((e2, e3))
+            counts.append(cnt.clone())
+
+    # the first dense pass gives v its scale; c is then fixed for the run
+    fa.fasgd_apply_updates(st, pool[:K], clients[:K], ts[:K])
+    torch.cuda.synchronize()
+    c = calibrate_c(v, f)
+    print(f"# c = {c:.6g} for transmit fraction {f}", file=sys.stderr, flush=True)
+    for i in range(warm):
+        step(False, c)
+    torch.cuda.synchronize()
+    print(f"# warmup done ({warm} steps)", file=sys.stderr, flush=True)
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(True, c)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    print(f"# timed {steps} steps in {wall:.3f} s", file=sys.stderr, flush=True)
+
+    ms = {k: [a.elapsed_time(b_) for a, b_ in pairs] for k, pairs in ev.items()}
+    m_list = [int(x.item()) for x in counts]
+    m_avg = float(np.mean(m_list))
+    updates = steps * P * K + sum(m_list)
+    value = updates / wall
+    dense_ms = float(np.mean(ms["dense"]))
+    dense_bytes = P * (36 + 4 * K)          # per launch: state 16 B read + 16 B write + 4 B last_T, 4 B per gradient
+    achieved = dense_bytes / (dense_ms * 1e-3) / 1e9
+    traffic = measured_traffic(P, K)
+    sel_ms, sp_ms = float(np.mean(ms["select"])), float(np.mean(ms["sparse"]))
+    sel_bytes = P * 8 + m_avg * 8                   # v + g read, (idx, val) written
+    sp_bytes = m_avg * 44                           # idx, val + 16 B state gather, 16 B scatter, 4 B last_T
+
+    # SASGD mode of the same pass, measured after the timed region
+    sas_ms = []
+    for r in range(3):
+        a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        base = st.T
+        a.record()
+        fa.sasgd_apply_updates(st, pool[:K], clients[base:base + K], ts[base:base + K])
+        b_.record()
+        torch.cuda.synchronize()
+        sas_ms.append(a.elapsed_time(b_))
+    sas_ms_avg = float(np.mean(sas_ms[1:]))
+    sas_bytes = P * (12 + 4 * K)
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "param-updates/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warm,
+        "ms_per_step": wall / steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {w.name}, P={P}, lambda={w.lam}, K={K} fused FASGD "
+                               f"updates + 1 B-FASGD push at ~{int(f * 100)}% per step, {args.math} math",
+                   "P": P, "K": K, "lambda": w.lam, "math": args.math, "transmit_fraction": f, "c": c},
+        "roofline": {"bound": "hbm", "kernel": "fasgd_dense_vec", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic, "algorithmic_bytes": dense_bytes},
+        "kernels": {
+            "fasgd_apply_updates": {"ms": dense_ms, "GB/s": achieved,
+                                    "param_updates_per_s": P * K / (dense_ms * 1e-3)},
+            "bfasgd_select_compact": {"ms": sel_ms, "GB/s": sel_bytes / (sel_ms * 1e-3) / 1e9,
+                                      "transmitted_fraction": m_avg / P},
+            "bfasgd_apply_sparse": {"ms": sp_ms, "GB/s_algorithmic": sp_bytes / (sp_ms * 1e-3) / 1e9},
+            "sasgd_apply_updates": {"ms": sas_ms_avg, "GB/s": sas_bytes / (sas_ms_avg * 1e-3) / 1e9},
+        },
+    }
+    if args.cpu_params:
+        P_s = min(args.cpu_params, P)
+        rate, dt, m_s = cpu_baseline(pool, theta0_host, clients, ts, c, w, K, P_s)
+        out["cpu_baseline"] = {"value": rate, "unit": "param-updates/s", "cores": 1, "kind": "oracle",
+                               "sample": f"first {P_s} parameters of the same workload, one step "
+                                         f"({K} dense updates + 1 push, {m_s} transmitted), {dt:.1f} s"}
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,190 @@
+/*
+ * fasgd.h -- C ABI of libfasgd.so, the parameter-server hot path of
+ * "Faster Asynchronous SGD" (A. Odena, arXiv:1601.04033) on one AMD
+ * Instinct MI355X (gfx950).
+ *
+ * Notation (Sec. 2.1): lambda clients, mu minibatch size, alpha master
+ * learning rate, T server timestamp (starts at 0, +1 per weight update),
+ * tau = T - j the step-staleness of a gradient computed on parameters with
+ * timestamp j.
+ *
+ * Conventions shared by every entry point
+ *   - Device memory is owned by the caller (allocated e.g. with torch); the
+ *     library keeps no pointer beyond a call and allocates nothing.
+ *   - Every call is asynchronous on `stream` (0 = the null stream) and never
+ *     synchronises the host.  Results are visible after the stream is
+ *     synchronised.
+ *   - All arguments are checked on the host before anything is enqueued.
+ *     On any error nothing is enqueued and the state (including T) is
+ *     unchanged; fasgd_last_error() then describes the problem.
+ *   - Device arrays are plain, densely packed 1-D arrays of P elements in
+ *     parameter order (structure of arrays).  4-byte alignment is required;
+ *     16-byte alignment of every array (as torch allocations have) selects
+ *     the vectorised kernels.
+ *   - Calls that share a state must be issued on one stream (or otherwise
+ *     ordered by the caller); concurrent calls on one state race.
+ */
+#ifndef FASGD_H
+#define FASGD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FASGD_MAX_K 64          /* most gradients one fused apply accepts */
+
+typedef enum fasgd_status {
+    FASGD_OK = 0,
+    FASGD_ERR_NULL = 1,         /* a required pointer is NULL */
+    FASGD_ERR_ARG = 2,          /* a size, count, timestamp or hyper-parameter is out of range */
+    FASGD_ERR_STALENESS = 3,    /* a gradient timestamp is later than the update it is applied at */
+    FASGD_ERR_CLIENT = 4,       /* a client id is outside [0, lambda) */
+    FASGD_ERR_ALIGN = 5,        /* a device pointer is not 4-byte aligned */
+    FASGD_ERR_CAPACITY = 6,     /* the B-FASGD workspace is smaller than bfasgd_workspace_bytes(P) */
+    FASGD_ERR_HIP = 7           /* the HIP runtime refused a launch */
+} fasgd_status;
+
+typedef enum fasgd_math {
+    FASGD_MATH_IEEE = 0,        /* correctly rounded fp32 sqrt and divisions */
+    FASGD_MATH_FAST = 1         /* hardware reciprocal square root and reciprocal (about 1 ulp each) */
+} fasgd_math;
+
+/*
+ * Server state (Sec. 2.2).  A host-side POD owned by the caller; the device
+ * arrays it points to are owned by the caller too.
+ *   theta   parameters theta, fp32 [P]
+ *   n       moving average of the squared gradient, fp32 [P]
+ *   b       moving average of the gradient, fp32 [P]
+ *   v       moving average of 1/sqrt(n - b^2 + eps), fp32 [P]
+ *   last_T  timestamp of the last update that touched each parameter,
+ *           int32 [P], -1 before the first
+ * Hyper-parameters: alpha (Sec. 2.1), gamma, beta, eps (Sec. 2.2).
+ * lambda bounds the client ids; mu is recorded only (a gradient arrives as
+ * the minibatch mean, Sec. 2.2).  T is advanced by the apply calls.
+ */
+typedef struct fasgd_state {
+    int64_t P;
+    int32_t lambda;
+    int32_t mu;
+    float alpha;
+    float gamma;
+    float beta;
+    float eps;
+    int32_t math_mode;          /* fasgd_math */
+    int32_t reserved;           /* 0 */
+    int64_t T;
+    float* theta;
+    float* n;
+    float* b;
+    float* v;
+    int32_t* last_T;
+} fasgd_state;
+
+/*
+ * Initialise a server (the FRED Server initialisation function, Sec. 3):
+ * fills n, b and v with n0, b0, v0 and last_T with -1 on `stream`, sets
+ * T = 0 (Sec. 2.1) and records the hyper-parameters in *st.  theta must
+ * already hold the initial parameters; it is not written.
+ * Requires P >= 1, lambda >= 1, mu >= 1, alpha > 0, gamma and beta in
+ * [0, 1], eps > 0 (finite), math_mode a fasgd_math value.
+ * n, b, v may be NULL for a state used only with sasgd_apply_updates.
+ */
+fasgd_status fasgd_init_state(fasgd_state* st, int64_t P, int32_t lambda, int32_t mu,
+                              float alpha, float gamma, float beta, float eps, int32_t math_mode,
+                              float n0, float b0, float v0,
+                              float* theta, float* n, float* b, float* v, int32_t* last_T,
+                              hipStream_t stream);
+
+/*
+ * FASGD apply-update for K client gradients in arrival order (Sec. 2.2):
+ * the k-th gradient is applied at server timestamp T + k with staleness
+ * tau_k = T + k - grad_ts[k], and for every parameter
+ *   n <- gamma n + (1 - gamma) g^2,   b <- gamma b + (1 - gamma) g,
+ *   v <- beta v + (1 - beta) / sqrt(max(n - b^2, 0) + eps),
+ *   theta <- theta - alpha / (v max(tau_k, 1)) g,
+ * one gradient after the other (the server lock serialises arrivals,
+ * Sec. 2.1), with each parameter's state held in registers across the K
+ * gradients.  last_T becomes T + K - 1 and T advances by K.
+ *   grads    host array of K device pointers, each fp32 [P]
+ *   clients  host int32 [K], each in [0, lambda)
+ *   grad_ts  host int64 [K], 0 <= grad_ts[k] <= T + k
+ *   K        1 .. FASGD_MAX_K
+ * Errors: FASGD_ERR_STALENESS if some grad_ts[k] > T + k; FASGD_ERR_ARG if
+ * K is out of range or T + K - 1 exceeds INT32_MAX (last_T is int32).
+ */
+fasgd_status fasgd_apply_updates(fasgd_state* st, const float* const* grads, const int32_t* clients,
+                                 const int64_t* grad_ts, int32_t K, hipStream_t stream);
+
+/*
+ * SASGD apply-update (staleness-aware ASGD, Sec. 1 and 2.1): the rate of
+ * the k-th gradient is alpha / max(tau_k, 1), theta <- theta - that * g.
+ * Reads and writes theta and last_T only (n, b, v may be NULL).  Same
+ * arguments, order and errors as fasgd_apply_updates.
+ */
+fasgd_status sasgd_apply_updates(fasgd_state* st, const float* const* grads, const int32_t* clients,
+                                 const int64_t* grad_ts, int32_t K, hipStream_t stream);
+
+/* Bytes of device workspace bfasgd_select_compact needs for P parameters. */
+size_t bfasgd_workspace_bytes(int64_t P);
+
+/*
+ * B-FASGD push selection and compaction (Sec. 2.3, decided per parameter,
+ * the per-parameter direction of Sec. 5).  Parameter j of this push is
+ * transmitted iff r_j < 1 / (1 + c / (v_j + eps_c)), decided in fp32 as
+ *   t = v_j + eps_c,  u = t + c,  transmit <=> r_j * u - t < 0 (one rounding),
+ * where r_j is the top 24 bits of word (j mod 4) of Philox4x32-10 at counter
+ * (j/4 low 32 bits, j/4 high 32 bits, T, client) with key (seed low, seed
+ * high), scaled by 2^-24 into [0, 1).  v is read from the state as it is
+ * before this push is applied.
+ * The transmitted entries are written in ascending index order:
+ * out_idx[i] = j (int32), out_val[i] = grad[j] (bit copy), for the first
+ * min(m, capacity) of them; *d_count (device int64) receives m, the number
+ * transmitted, even when m > capacity.  capacity >= P never truncates.
+ *   grad       device fp32 [P], this client's gradient
+ *   c, eps_c   finite, >= 0
+ *   T          server timestamp this push is applied at, 0 <= T < 2^32
+ *   client     in [0, lambda)
+ *   workspace  device scratch of at least bfasgd_workspace_bytes(P) bytes,
+ *              256-byte aligned; its contents need no initialisation
+ * Requires P <= INT32_MAX (int32 indices).  The selection is deterministic:
+ * it does not depend on launch shape, timing or earlier calls.
+ */
+fasgd_status bfasgd_select_compact(const fasgd_state* st, const float* grad, float c, float eps_c,
+                                   uint64_t seed, int64_t T, int32_t client,
+                                   int32_t* out_idx, float* out_val, int64_t capacity,
+                                   int64_t* d_count, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream);
+
+/*
+ * Server side of a B-FASGD push: the FASGD update of fasgd_apply_updates,
+ * applied at timestamp T with staleness T - grad_ts, to the listed
+ * parameters only, with g = val[i] for parameter idx[i], for
+ * i < min(*d_count, capacity) (*d_count is read on the device, so this can
+ * follow bfasgd_select_compact on the same stream without a host
+ * round-trip).  Unlisted parameters keep theta, n, b, v and last_T; listed
+ * ones get last_T = T.  T advances by one even when the list is empty.
+ * Indices must be distinct; an index outside [0, P) is skipped.
+ *   idx, val  device int32 / fp32 [capacity]
+ *   d_count   device int64 [1]
+ * Errors: as fasgd_apply_updates with K = 1.
+ */
+fasgd_status bfasgd_apply_sparse(fasgd_state* st, const int32_t* idx, const float* val,
+                                 const int64_t* d_count, int64_t capacity, int32_t client,
+                                 int64_t grad_ts, hipStream_t stream);
+
+/* Static text naming a status code. */
+const char* fasgd_status_string(fasgd_status s);
+
+/* Text describing the last error returned on the calling thread ("" if none). */
+const char* fasgd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FASGD_H */

@@ -1,0 +1,234 @@
+"""Python binding of libfasgd.so: the FASGD parameter-server hot path of
+"Faster Asynchronous SGD" (arXiv:1601.04033) on an MI355X.
+
+Argument marshalling only.  Every step runs in the HIP kernels of
+libfasgd.so; torch provides device memory and the stream.  The functions
+keep the C ABI's names (include/fasgd.h):
+
+    fasgd_init_state, fasgd_apply_updates, sasgd_apply_updates,
+    bfasgd_workspace_bytes, bfasgd_select_compact, bfasgd_apply_sparse
+
+There is no fallback: if libfasgd.so is missing or cannot be loaded, every
+call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfasgd.so")
+
+FASGD_MAX_K = 64
+MATH_IEEE = 0
+MATH_FAST = 1
+
+STATUS = {0: "FASGD_OK", 1: "FASGD_ERR_NULL", 2: "FASGD_ERR_ARG", 3: "FASGD_ERR_STALENESS",
+          4: "FASGD_ERR_CLIENT", 5: "FASGD_ERR_ALIGN", 6: "FASGD_ERR_CAPACITY", 7: "FASGD_ERR_HIP"}
+
+# every function include/fasgd.h declares
+ABI_FUNCTIONS = ("fasgd_init_state", "fasgd_apply_updates", "sasgd_apply_updates",
+                 "bfasgd_workspace_bytes", "bfasgd_select_compact", "bfasgd_apply_sparse",
+                 "fasgd_status_string", "fasgd_last_error")
+
+
+class FasgdError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+class fasgd_state(ctypes.Structure):
+    """Mirror of the C struct fasgd_state."""
+    _fields_ = [("P", ctypes.c_int64), ("lambda_", ctypes.c_int32), ("mu", ctypes.c_int32),
+                ("alpha", ctypes.c_float), ("gamma", ctypes.c_float), ("beta", ctypes.c_float),
+                ("eps", ctypes.c_float), ("math_mode", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("T", ctypes.c_int64),
+                ("theta", ctypes.c_void_p), ("n", ctypes.c_void_p), ("b", ctypes.c_void_p),
+                ("v", ctypes.c_void_p), ("last_T", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def load_library(path: Optional[str] = None):
+    """Load libfasgd.so (raises OSError if it is missing: no fallback)."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise OSError(f"{p} is not built; run __graft_entry__.build() (hipcc, gfx950)")
+    lib = ctypes.CDLL(p)
+    S, P = ctypes.POINTER(fasgd_state), ctypes.c_void_p
+    i32, i64, f, u64, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_uint64, ctypes.c_size_t
+    lib.fasgd_init_state.argtypes = [S, i64, i32, i32, f, f, f, f, i32, f, f, f, P, P, P, P, P, P]
+    lib.fasgd_apply_updates.argtypes = [S, P, P, P, i32, P]
+    lib.sasgd_apply_updates.argtypes = [S, P, P, P, i32, P]
+    lib.bfasgd_workspace_bytes.argtypes = [i64]
+    lib.bfasgd_workspace_bytes.restype = sz
+    lib.bfasgd_select_compact.argtypes = [S, P, f, f, u64, i64, i32, P, P, i64, P, P, sz, P]
+    lib.bfasgd_apply_sparse.argtypes = [S, P, P, P, i64, i32, i64, P]
+    for name in ("fasgd_init_state", "fasgd_apply_updates", "sasgd_apply_updates",
+                 "bfasgd_select_compact", "bfasgd_apply_sparse"):
+        getattr(lib, name).restype = ctypes.c_int
+    lib.fasgd_status_string.argtypes = [ctypes.c_int]
+    lib.fasgd_status_string.restype = ctypes.c_char_p
+    lib.fasgd_last_error.argtypes = []
+    lib.fasgd_last_error.restype = ctypes.c_char_p
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise FasgdError(rc, load_library().fasgd_last_error().decode())
+
+
+def _stream(stream) -> int:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _dev_ptr(t, dtype, name, allow_none=False):
+    import torch
+    if t is None:
+        if allow_none:
+            return None
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype or not t.is_contiguous():
+        raise TypeError(f"{name} must be a contiguous {dtype} tensor")
+    return t.data_ptr()
+
+
+class State:
+    """A server state: the C struct plus the tensors it points to (kept alive here)."""
+
+    def __init__(self, c: fasgd_state, tensors: dict):
+        self.c = c
+        self.tensors = tensors
+
+    @property
+    def T(self) -> int:
+        return int(self.c.T)
+
+    @property
+    def P(self) -> int:
+        return int(self.c.P)
+
+    def __getattr__(self, name):
+        t = self.__dict__.get("tensors", {})
+        if name in t:
+            return t[name]
+        raise AttributeError(name)
+
+
+def fasgd_init_state(theta, n, b, v, last_T, *, lam: int, mu: int = 1, alpha: float,
+                     gamma: float = 0.95, beta: float = 0.9, eps: float = 1e-4,
+                     math_mode: int = MATH_FAST, n0: float = 0.0, b0: float = 0.0, v0: float = 0.0,
+                     stream=None) -> State:
+    """theta (holding theta0), n, b, v: fp32 [P]; last_T: int32 [P].  n, b, v may be None (SASGD only)."""
+    import torch
+    P = theta.numel()
+    for name, t in (("n", n), ("b", b), ("v", v), ("last_T", last_T)):
+        if t is not None and t.numel() != P:
+            raise ValueError(f"{name} has {t.numel()} elements, theta has {P}")
+    st = fasgd_state()
+    rc = load_library().fasgd_init_state(
+        ctypes.byref(st), P, lam, mu, alpha, gamma, beta, eps, math_mode, n0, b0, v0,
+        _dev_ptr(theta, torch.float32, "theta"), _dev_ptr(n, torch.float32, "n", True),
+        _dev_ptr(b, torch.float32, "b", True), _dev_ptr(v, torch.float32, "v", True),
+        _dev_ptr(last_T, torch.int32, "last_T"), _stream(stream))
+    _check(rc)
+    return State(st, dict(theta=theta, n=n, b=b, v=v, last_T=last_T))
+
+
+def _dense_args(state: State, grads: Sequence, clients: Sequence[int], grad_ts: Sequence[int]):
+    import torch
+    K = len(grads)
+    if len(clients) != K or len(grad_ts) != K:
+        raise ValueError("grads, clients and grad_ts must have the same length")
+    if not 1 <= K <= FASGD_MAX_K:
+        raise ValueError(f"K = {K} is not in [1, {FASGD_MAX_K}]")
+    ptrs = (ctypes.c_void_p * K)()
+    for k, g in enumerate(grads):
+        if g.numel() != state.P:
+            raise ValueError(f"grads[{k}] has {g.numel()} elements, P = {state.P}")
+        ptrs[k] = _dev_ptr(g, torch.float32, f"grads[{k}]")
+    c = (ctypes.c_int32 * K)(*[int(x) for x in clients])
+    ts = (ctypes.c_int64 * K)(*[int(x) for x in grad_ts])
+    return ptrs, c, ts, K
+
+
+def fasgd_apply_updates(state: State, grads: Sequence, clients: Sequence[int], grad_ts: Sequence[int],
+                        stream=None) -> None:
+    """Apply K gradients (arrival order) with the FASGD rule; T advances by K."""
+    ptrs, c, ts, K = _dense_args(state, grads, clients, grad_ts)
+    _check(load_library().fasgd_apply_updates(ctypes.byref(state.c), ptrs, c, ts, K, _stream(stream)))
+
+
+def sasgd_apply_updates(state: State, grads: Sequence, clients: Sequence[int], grad_ts: Sequence[int],
+                        stream=None) -> None:
+    """Apply K gradients with the SASGD rate alpha / max(tau, 1); T advances by K."""
+    ptrs, c, ts, K = _dense_args(state, grads, clients, grad_ts)
+    _check(load_library().sasgd_apply_updates(ctypes.byref(state.c), ptrs, c, ts, K, _stream(stream)))
+
+
+def bfasgd_workspace_bytes(P: int) -> int:
+    return int(load_library().bfasgd_workspace_bytes(int(P)))
+
+
+def bfasgd_select_compact(state: State, grad, c: float, eps_c: float, seed: int, T: int, client: int,
+                          out_idx, out_val, d_count, workspace, stream=None) -> None:
+    """Per-parameter send/skip selection of one client gradient, compacted
+    into out_idx (int32) / out_val (fp32) in ascending index order; the
+    number transmitted goes to d_count (int64 [1], device)."""
+    import torch
+    cap = out_idx.numel()
+    if out_val.numel() != cap:
+        raise ValueError("out_idx and out_val must have the same capacity")
+    if grad.numel() != state.P:
+        raise ValueError("grad length differs from P")
+    rc = load_library().bfasgd_select_compact(
+        ctypes.byref(state.c), _dev_ptr(grad, torch.float32, "grad"), c, eps_c,
+        int(seed) & (2 ** 64 - 1), int(T), int(client),
+        _dev_ptr(out_idx, torch.int32, "out_idx"), _dev_ptr(out_val, torch.float32, "out_val"), cap,
+        _dev_ptr(d_count, torch.int64, "d_count"), _dev_ptr(workspace, torch.uint8, "workspace"),
+        workspace.numel(), _stream(stream))
+    _check(rc)
+
+
+def bfasgd_apply_sparse(state: State, idx, val, d_count, client: int, grad_ts: int, stream=None) -> None:
+    """FASGD update of the listed parameters (first *d_count entries); T advances by one."""
+    import torch
+    cap = idx.numel()
+    if val.numel() != cap:
+        raise ValueError("idx and val must have the same capacity")
+    rc = load_library().bfasgd_apply_sparse(
+        ctypes.byref(state.c), _dev_ptr(idx, torch.int32, "idx"), _dev_ptr(val, torch.float32, "val"),
+        _dev_ptr(d_count, torch.int64, "d_count"), cap, int(client), int(grad_ts), _stream(stream))
+    _check(rc)
+
+
+def allocate_state(P: int, device="cuda", with_stats: bool = True):
+    """Device tensors for a state of P parameters (torch allocations are
+    256-byte aligned, so the vectorised kernels are used)."""
+    import torch
+    f = dict(device=device, dtype=torch.float32)
+    theta = torch.empty(P, **f)
+    n = torch.empty(P, **f) if with_stats else None
+    b = torch.empty(P, **f) if with_stats else None
+    v = torch.empty(P, **f) if with_stats else None
+    last_T = torch.empty(P, device=device, dtype=torch.int32)
+    return theta, n, b, v, last_T
+
+
+def allocate_workspace(P: int, device="cuda"):
+    import torch
+    return torch.empty(bfasgd_workspace_bytes(P), device=device, dtype=torch.uint8)

@@ -1,0 +1,293 @@
+// C ABI of libfasgd.so (declared in include/fasgd.h): host-side argument
+// checks, step-staleness bookkeeping (Sec. 2.1) and kernel dispatch.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "../../include/fasgd.h"
+#include "kernels.hpp"
+
+static_assert(FASGD_MAX_K == fasgd::kMaxK, "K limit mismatch");
+
+namespace {
+
+thread_local char g_err[512];
+
+fasgd_status fail(fasgd_status s, const char* fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+fasgd_status ok()
+{
+    g_err[0] = '\0';
+    return FASGD_OK;
+}
+
+fasgd_status hip_fail(hipError_t e, const char* what)
+{
+    return fail(FASGD_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+fasgd_status check_state(const fasgd_state* st, bool need_stats)
+{
+    if (!st) return fail(FASGD_ERR_NULL, "state is NULL");
+    if (st->P < 1) return fail(FASGD_ERR_ARG, "P = %lld must be >= 1", (long long)st->P);
+    if (st->lambda < 1) return fail(FASGD_ERR_ARG, "lambda = %d must be >= 1", st->lambda);
+    if (st->T < 0 || st->T > INT32_MAX) return fail(FASGD_ERR_ARG, "T = %lld out of range", (long long)st->T);
+    if (!st->theta || !st->last_T) return fail(FASGD_ERR_NULL, "theta or last_T is NULL");
+    if (need_stats && (!st->n || !st->b || !st->v)) return fail(FASGD_ERR_NULL, "n, b or v is NULL");
+    if (!aligned(st->theta, 4) || !aligned(st->last_T, 4) || (st->n && !aligned(st->n, 4)) ||
+        (st->b && !aligned(st->b, 4)) || (st->v && !aligned(st->v, 4)))
+        return fail(FASGD_ERR_ALIGN, "state arrays must be 4-byte aligned");
+    if (need_stats && st->math_mode != FASGD_MATH_IEEE && st->math_mode != FASGD_MATH_FAST)
+        return fail(FASGD_ERR_ARG, "math_mode = %d is not a fasgd_math value", st->math_mode);
+    return FASGD_OK;
+}
+
+fasgd::Hyper hyper_of(const fasgd_state* st)
+{
+    fasgd::Hyper h;
+    h.gamma = st->gamma;
+    h.omg = 1.0f - st->gamma;
+    h.beta = st->beta;
+    h.omb = 1.0f - st->beta;
+    h.eps = st->eps;
+    h.alpha = st->alpha;
+    return h;
+}
+
+// tau = (T + k) - grad_ts[k] >= 0; the divisor is max(tau, 1).
+fasgd_status staleness(const fasgd_state* st, const int32_t* clients, const int64_t* grad_ts, int32_t K,
+                       float* tau_div)
+{
+    for (int32_t k = 0; k < K; ++k) {
+        const int64_t Tk = st->T + k;
+        if (clients[k] < 0 || clients[k] >= st->lambda)
+            return fail(FASGD_ERR_CLIENT, "clients[%d] = %d is outside [0, %d)", k, clients[k], st->lambda);
+        if (grad_ts[k] < 0 || grad_ts[k] > Tk)
+            return fail(FASGD_ERR_STALENESS, "grad_ts[%d] = %lld is not in [0, T + k = %lld]", k,
+                        (long long)grad_ts[k], (long long)Tk);
+        const int64_t tau = Tk - grad_ts[k];
+        tau_div[k] = static_cast<float>(tau > 0 ? tau : 1);
+    }
+    return FASGD_OK;
+}
+
+fasgd_status dense_common(fasgd_state* st, const float* const* grads, const int32_t* clients,
+                          const int64_t* grad_ts, int32_t K, bool fasgd_mode, fasgd::DenseArgs& a, bool& vec)
+{
+    fasgd_status s = check_state(st, fasgd_mode);
+    if (s != FASGD_OK) return s;
+    if (!grads || !clients || !grad_ts) return fail(FASGD_ERR_NULL, "grads, clients or grad_ts is NULL");
+    if (K < 1 || K > FASGD_MAX_K) return fail(FASGD_ERR_ARG, "K = %d is not in [1, %d]", K, FASGD_MAX_K);
+    if (st->T + K - 1 > INT32_MAX) return fail(FASGD_ERR_ARG, "T + K - 1 exceeds the int32 last_T range");
+    float tau_div[FASGD_MAX_K];
+    s = staleness(st, clients, grad_ts, K, tau_div);
+    if (s != FASGD_OK) return s;
+    vec = aligned(st->theta, 16) && aligned(st->last_T, 16) &&
+          (!fasgd_mode || (aligned(st->n, 16) && aligned(st->b, 16) && aligned(st->v, 16)));
+    memset(&a, 0, sizeof a);
+    for (int32_t k = 0; k < K; ++k) {
+        if (!grads[k]) return fail(FASGD_ERR_NULL, "grads[%d] is NULL", k);
+        if (!aligned(grads[k], 4)) return fail(FASGD_ERR_ALIGN, "grads[%d] is not 4-byte aligned", k);
+        vec = vec && aligned(grads[k], 16);
+        a.grad[k] = grads[k];
+        const bool rate = !fasgd_mode || st->math_mode == FASGD_MATH_FAST;
+        a.coef[k] = rate ? st->alpha / tau_div[k] : tau_div[k];
+    }
+    a.theta = st->theta;
+    a.n = st->n;
+    a.b = st->b;
+    a.v = st->v;
+    a.last_T = st->last_T;
+    a.P = st->P;
+    a.K = K;
+    a.last_T_value = static_cast<int32_t>(st->T + K - 1);
+    a.h = hyper_of(st);
+    return FASGD_OK;
+}
+
+bool finite_nonneg(float x) { return isfinite(x) && x >= 0.0f; }
+
+}  // namespace
+
+extern "C" {
+
+fasgd_status fasgd_init_state(fasgd_state* st, int64_t P, int32_t lambda, int32_t mu, float alpha,
+                              float gamma, float beta, float eps, int32_t math_mode, float n0, float b0,
+                              float v0, float* theta, float* n, float* b, float* v, int32_t* last_T,
+                              hipStream_t stream)
+{
+    if (!st) return fail(FASGD_ERR_NULL, "state is NULL");
+    if (P < 1) return fail(FASGD_ERR_ARG, "P = %lld must be >= 1", (long long)P);
+    if (lambda < 1 || mu < 1) return fail(FASGD_ERR_ARG, "lambda and mu must be >= 1");
+    if (!(isfinite(alpha) && alpha > 0.0f)) return fail(FASGD_ERR_ARG, "alpha must be finite and > 0");
+    if (!(gamma >= 0.0f && gamma <= 1.0f) || !(beta >= 0.0f && beta <= 1.0f))
+        return fail(FASGD_ERR_ARG, "gamma and beta must be in [0, 1]");
+    if (!(isfinite(eps) && eps > 0.0f)) return fail(FASGD_ERR_ARG, "eps must be finite and > 0");
+    if (math_mode != FASGD_MATH_IEEE && math_mode != FASGD_MATH_FAST)
+        return fail(FASGD_ERR_ARG, "math_mode = %d is not a fasgd_math value", math_mode);
+    if (!isfinite(n0) || !isfinite(b0) || !isfinite(v0)) return fail(FASGD_ERR_ARG, "n0, b0, v0 must be finite");
+    if (!theta || !last_T) return fail(FASGD_ERR_NULL, "theta or last_T is NULL");
+    if ((n || b || v) && !(n && b && v)) return fail(FASGD_ERR_NULL, "n, b and v must be all set or all NULL");
+    if (!aligned(theta, 4) || !aligned(last_T, 4) || (n && (!aligned(n, 4) || !aligned(b, 4) || !aligned(v, 4))))
+        return fail(FASGD_ERR_ALIGN, "state arrays must be 4-byte aligned");
+    const hipError_t e = fasgd::launch_init(n, b, v, last_T, P, n0, b0, v0, stream);
+    if (e != hipSuccess) return hip_fail(e, "fasgd_init_state");
+    fasgd_state s;
+    memset(&s, 0, sizeof s);
+    s.P = P;
+    s.lambda = lambda;
+    s.mu = mu;
+    s.alpha = alpha;
+    s.gamma = gamma;
+    s.beta = beta;
+    s.eps = eps;
+    s.math_mode = math_mode;
+    s.T = 0;
+    s.theta = theta;
+    s.n = n;
+    s.b = b;
+    s.v = v;
+    s.last_T = last_T;
+    *st = s;
+    return ok();
+}
+
+fasgd_status fasgd_apply_updates(fasgd_state* st, const float* const* grads, const int32_t* clients,
+                                 const int64_t* grad_ts, int32_t K, hipStream_t stream)
+{
+    fasgd::DenseArgs a;
+    bool vec = false;
+    fasgd_status s = dense_common(st, grads, clients, grad_ts, K, true, a, vec);
+    if (s != FASGD_OK) return s;
+    const hipError_t e = fasgd::launch_fasgd_dense(a, st->math_mode, vec, stream);
+    if (e != hipSuccess) return hip_fail(e, "fasgd_apply_updates");
+    st->T += K;
+    return ok();
+}
+
+fasgd_status sasgd_apply_updates(fasgd_state* st, const float* const* grads, const int32_t* clients,
+                                 const int64_t* grad_ts, int32_t K, hipStream_t stream)
+{
+    fasgd::DenseArgs a;
+    bool vec = false;
+    fasgd_status s = dense_common(st, grads, clients, grad_ts, K, false, a, vec);
+    if (s != FASGD_OK) return s;
+    const hipError_t e = fasgd::launch_sasgd_dense(a, vec, stream);
+    if (e != hipSuccess) return hip_fail(e, "sasgd_apply_updates");
+    st->T += K;
+    return ok();
+}
+
+size_t bfasgd_workspace_bytes(int64_t P)
+{
+    if (P < 1) return 0;
+    return fasgd::select_workspace_bytes(P);
+}
+
+fasgd_status bfasgd_select_compact(const fasgd_state* st, const float* grad, float c, float eps_c, uint64_t seed,
+                                   int64_t T, int32_t client, int32_t* out_idx, float* out_val, int64_t capacity,
+                                   int64_t* d_count, void* workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    if (!st) return fail(FASGD_ERR_NULL, "state is NULL");
+    if (st->P < 1 || st->P > INT32_MAX) return fail(FASGD_ERR_ARG, "P must be in [1, INT32_MAX] for int32 indices");
+    if (st->lambda < 1) return fail(FASGD_ERR_ARG, "lambda = %d must be >= 1", st->lambda);
+    if (!st->v || !grad || !d_count || !workspace) return fail(FASGD_ERR_NULL, "v, grad, d_count or workspace is NULL");
+    if (capacity < 0) return fail(FASGD_ERR_ARG, "capacity must be >= 0");
+    if (capacity > 0 && (!out_idx || !out_val)) return fail(FASGD_ERR_NULL, "out_idx or out_val is NULL");
+    if (!finite_nonneg(c) || !finite_nonneg(eps_c)) return fail(FASGD_ERR_ARG, "c and eps_c must be finite and >= 0");
+    if (T < 0 || T > int64_t(UINT32_MAX)) return fail(FASGD_ERR_ARG, "T = %lld is not in [0, 2^32)", (long long)T);
+    if (client < 0 || client >= st->lambda)
+        return fail(FASGD_ERR_CLIENT, "client = %d is outside [0, %d)", client, st->lambda);
+    if (!aligned(st->v, 4) || !aligned(grad, 4) || (out_idx && !aligned(out_idx, 4)) ||
+        (out_val && !aligned(out_val, 4)) || !aligned(d_count, 8))
+        return fail(FASGD_ERR_ALIGN, "misaligned v, grad, output list or d_count");
+    if (!aligned(workspace, 256)) return fail(FASGD_ERR_ALIGN, "workspace must be 256-byte aligned");
+    if (workspace_bytes < fasgd::select_workspace_bytes(st->P))
+        return fail(FASGD_ERR_CAPACITY, "workspace of %zu bytes is smaller than the %zu needed", workspace_bytes,
+                    fasgd::select_workspace_bytes(st->P));
+    fasgd::SelectArgs a;
+    memset(&a, 0, sizeof a);
+    a.v = st->v;
+    a.grad = grad;
+    a.out_idx = out_idx;
+    a.out_val = out_val;
+    a.d_count = d_count;
+    a.P = st->P;
+    a.capacity = capacity;
+    a.c = c;
+    a.eps_c = eps_c;
+    a.key0 = static_cast<uint32_t>(seed);
+    a.key1 = static_cast<uint32_t>(seed >> 32);
+    a.ctr_T = static_cast<uint32_t>(T);
+    a.ctr_client = static_cast<uint32_t>(client);
+    fasgd::select_workspace_layout(workspace, st->P, a);
+    const bool vec = aligned(st->v, 16) && aligned(grad, 16);
+    const hipError_t e = fasgd::launch_select(a, vec, stream);
+    if (e != hipSuccess) return hip_fail(e, "bfasgd_select_compact");
+    return ok();
+}
+
+fasgd_status bfasgd_apply_sparse(fasgd_state* st, const int32_t* idx, const float* val, const int64_t* d_count,
+                                 int64_t capacity, int32_t client, int64_t grad_ts, hipStream_t stream)
+{
+    fasgd_status s = check_state(st, true);
+    if (s != FASGD_OK) return s;
+    if (!d_count) return fail(FASGD_ERR_NULL, "d_count is NULL");
+    if (capacity < 0) return fail(FASGD_ERR_ARG, "capacity must be >= 0");
+    if (capacity > 0 && (!idx || !val)) return fail(FASGD_ERR_NULL, "idx or val is NULL");
+    if ((idx && !aligned(idx, 4)) || (val && !aligned(val, 4)) || !aligned(d_count, 8))
+        return fail(FASGD_ERR_ALIGN, "misaligned idx, val or d_count");
+    float tau_div;
+    s = staleness(st, &client, &grad_ts, 1, &tau_div);
+    if (s != FASGD_OK) return s;
+    fasgd::SparseArgs a;
+    memset(&a, 0, sizeof a);
+    a.theta = st->theta;
+    a.n = st->n;
+    a.b = st->b;
+    a.v = st->v;
+    a.last_T = st->last_T;
+    a.idx = idx;
+    a.val = val;
+    a.d_count = d_count;
+    a.capacity = capacity;
+    a.P = st->P;
+    a.coef = st->math_mode == FASGD_MATH_FAST ? st->alpha / tau_div : tau_div;
+    a.last_T_value = static_cast<int32_t>(st->T);
+    a.h = hyper_of(st);
+    if (capacity > 0) {
+        const hipError_t e = fasgd::launch_sparse(a, st->math_mode, stream);
+        if (e != hipSuccess) return hip_fail(e, "bfasgd_apply_sparse");
+    }
+    st->T += 1;
+    return ok();
+}
+
+const char* fasgd_status_string(fasgd_status s)
+{
+    switch (s) {
+    case FASGD_OK: return "ok";
+    case FASGD_ERR_NULL: return "null pointer";
+    case FASGD_ERR_ARG: return "argument out of range";
+    case FASGD_ERR_STALENESS: return "negative staleness (gradient timestamp after the update)";
+    case FASGD_ERR_CLIENT: return "client id outside [0, lambda)";
+    case FASGD_ERR_ALIGN: return "misaligned pointer";
+    case FASGD_ERR_CAPACITY: return "workspace too small";
+    case FASGD_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+const char* fasgd_last_error(void) { return g_err; }
+
+}  // extern "C"

@@ -1,0 +1,79 @@
+// Launchers of the device kernels, called by the C ABI after it has
+// validated every argument.  Each returns the HIP launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "device_math.hpp"
+
+namespace fasgd {
+
+constexpr int kMaxK = 64;
+
+// One fused pass of K gradients over the whole state.
+struct DenseArgs {
+    float* theta;
+    float* n;
+    float* b;
+    float* v;
+    int32_t* last_T;
+    const float* grad[kMaxK];
+    float coef[kMaxK];      // FASGD IEEE: tau_k; FASGD FAST and SASGD: alpha / tau_k
+    int64_t P;
+    int32_t K;
+    int32_t last_T_value;   // T + K - 1
+    Hyper h;
+};
+
+hipError_t launch_init(float* n, float* b, float* v, int32_t* last_T, int64_t P,
+                       float n0, float b0, float v0, hipStream_t s);
+hipError_t launch_fasgd_dense(const DenseArgs& a, int mode, bool aligned, hipStream_t s);
+hipError_t launch_sasgd_dense(const DenseArgs& a, bool aligned, hipStream_t s);
+
+// B-FASGD selection: Philox decisions -> per-wave ballots and per-tile
+// counts, an exclusive scan of the tile counts, then ordered writes.
+struct SelectArgs {
+    const float* v;
+    const float* grad;
+    int32_t* out_idx;
+    float* out_val;
+    int64_t* d_count;
+    uint64_t* ballots;      // 4 per 64 chunks of 4 parameters
+    uint32_t* tile_count;
+    uint32_t* tile_offset;
+    int64_t P;
+    int64_t capacity;
+    int64_t n_tiles;
+    float c;
+    float eps_c;
+    uint32_t key0, key1;    // seed low / high words
+    uint32_t ctr_T;         // counter word 2
+    uint32_t ctr_client;    // counter word 3
+};
+
+size_t select_workspace_bytes(int64_t P);
+// Carve the workspace into ballots / tile counts / tile offsets.
+void select_workspace_layout(void* ws, int64_t P, SelectArgs& a);
+hipError_t launch_select(const SelectArgs& a, bool aligned, hipStream_t s);
+
+struct SparseArgs {
+    float* theta;
+    float* n;
+    float* b;
+    float* v;
+    int32_t* last_T;
+    const int32_t* idx;
+    const float* val;
+    const int64_t* d_count;
+    int64_t capacity;
+    int64_t P;
+    float coef;             // as DenseArgs::coef for this one push
+    int32_t last_T_value;   // T
+    Hyper h;
+};
+
+hipError_t launch_sparse(const SparseArgs& a, int mode, hipStream_t s);
+
+}  // namespace fasgd

@@ -1,0 +1,190 @@
+"""The C ABI without a GPU: the library loads, exports every function the
+header declares, and its host-side checks reject bad arguments before any
+launch (so these calls never touch a device)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_1601_04033_amd as fa
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fasgd.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(fa.LIB_PATH):
+        from paper_1601_04033_amd import _build
+        _build.build()
+    return fa.load_library()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*([a-z_0-9]+)\s*\(", text, flags=re.M)))
+
+
+def test_header_and_binding_agree():
+    assert sorted(fa.ABI_FUNCTIONS) == _declared_functions()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    for code in range(8):
+        assert lib.fasgd_status_string(code)
+    assert lib.fasgd_status_string(99) == b"unknown status"
+
+
+def test_workspace_bytes(lib):
+    assert fa.bfasgd_workspace_bytes(0) == 0
+    small = fa.bfasgd_workspace_bytes(1)
+    assert small > 0 and small % 256 == 0
+    big = fa.bfasgd_workspace_bytes(1_000_000_000)
+    # 1 bit of ballot per parameter, padded to whole tiles, plus two words per tile
+    assert 1_000_000_000 / 8 <= big < 1_000_000_000 / 8 * 1.05
+
+
+class _Fake:
+    """16-byte aligned host buffers standing in for device pointers; the
+    calls below fail validation before any kernel could read them."""
+
+    def __init__(self, P):
+        self.bufs = [np.zeros(P + 8, np.float32) for _ in range(6)]
+
+    def ptr(self, i, misalign=0):
+        a = self.bufs[i]
+        p = a.ctypes.data
+        p = (p + 15) & ~15
+        return p + misalign
+
+
+def _state(P=16, lam=4, T=0):
+    f = _Fake(P)
+    st = fa.fasgd_state()
+    st.P, st.lambda_, st.mu = P, lam, 1
+    st.alpha, st.gamma, st.beta, st.eps = 0.01, 0.95, 0.9, 1e-4
+    st.math_mode, st.T = 1, T
+    st.theta, st.n, st.b, st.v, st.last_T = f.ptr(0), f.ptr(1), f.ptr(2), f.ptr(3), f.ptr(4)
+    return st, f
+
+
+def _call_dense(lib, fn, st, ts, clients=None, K=None, grads=None, fake=None):
+    K = len(ts) if K is None else K
+    g = (ctypes.c_void_p * max(K, 1))(*([fake.ptr(5)] * max(K, 1))) if grads is None else grads
+    c = (ctypes.c_int32 * max(K, 1))(*(clients or [0] * max(K, 1)))
+    t = (ctypes.c_int64 * max(K, 1))(*(ts or [0]))
+    return getattr(lib, fn)(ctypes.byref(st), g, c, t, K, None)
+
+
+@pytest.mark.parametrize("fn", ["fasgd_apply_updates", "sasgd_apply_updates"])
+def test_dense_rejects_bad_arguments(lib, fn):
+    st, f = _state(T=3)
+    # negative staleness: gradient timestamp after the update it is applied at
+    assert _call_dense(lib, fn, st, [4], fake=f) == 3
+    assert b"grad_ts[0]" in lib.fasgd_last_error()
+    assert _call_dense(lib, fn, st, [3, 5], fake=f) == 3          # T + 1 = 4 < 5
+    assert _call_dense(lib, fn, st, [-1], fake=f) == 3
+    # client outside [0, lambda)
+    assert _call_dense(lib, fn, st, [0], clients=[4], fake=f) == 4
+    assert _call_dense(lib, fn, st, [0], clients=[-1], fake=f) == 4
+    # K out of range
+    assert _call_dense(lib, fn, st, [0], K=0, fake=f) == 2
+    assert _call_dense(lib, fn, st, [0] * 65, K=65, fake=f) == 2
+    # null gradient pointer, null state arrays, misalignment
+    nullg = (ctypes.c_void_p * 1)(None)
+    assert _call_dense(lib, fn, st, [0], grads=nullg, fake=f) == 1
+    assert lib.fasgd_apply_updates(None, nullg, None, None, 1, None) == 1
+    bad, f2 = _state()
+    bad.theta = None
+    assert _call_dense(lib, fn, bad, [0], fake=f2) == 1
+    mis, f3 = _state()
+    mis.theta = f3.ptr(0, misalign=2)
+    assert _call_dense(lib, fn, mis, [0], fake=f3) == 5
+    # last_T is int32: T + K - 1 must fit
+    big, f4 = _state(T=2 ** 31 - 2)
+    assert _call_dense(lib, fn, big, [0, 0, 0], fake=f4) == 2
+    # nothing was applied
+    assert st.T == 3
+
+
+def test_fasgd_needs_statistics_but_sasgd_does_not_validate_them(lib):
+    st, f = _state(T=1)
+    st.n = None
+    assert _call_dense(lib, "fasgd_apply_updates", st, [5], fake=f) == 1   # n missing is checked first
+    assert _call_dense(lib, "sasgd_apply_updates", st, [5], fake=f) == 3   # n unused by SASGD
+    st.n = f.ptr(1)
+    st.math_mode = 7
+    assert _call_dense(lib, "fasgd_apply_updates", st, [0], fake=f) == 2
+
+
+def test_init_rejects_bad_arguments(lib):
+    f = _Fake(16)
+    st = fa.fasgd_state()
+    P4 = [f.ptr(i) for i in range(5)]
+
+    def init(P=16, lam=4, mu=1, alpha=0.01, gamma=0.95, beta=0.9, eps=1e-4, mode=1, ptrs=P4):
+        return lib.fasgd_init_state(ctypes.byref(st), P, lam, mu, alpha, gamma, beta, eps, mode,
+                                    0.0, 0.0, 0.0, *ptrs, None)
+
+    assert init(P=0) == 2
+    assert init(lam=0) == 2
+    assert init(alpha=0.0) == 2
+    assert init(alpha=float("nan")) == 2
+    assert init(gamma=1.5) == 2
+    assert init(beta=-0.1) == 2
+    assert init(eps=0.0) == 2
+    assert init(mode=2) == 2
+    assert init(ptrs=[None] + P4[1:]) == 1
+    assert init(ptrs=[P4[0], None, P4[2], P4[3], P4[4]]) == 1     # n, b, v all or none
+    assert init(ptrs=[P4[0] + 2] + P4[1:]) == 5
+    assert lib.fasgd_init_state(None, 16, 4, 1, 0.01, 0.95, 0.9, 1e-4, 1, 0.0, 0.0, 0.0, *P4, None) == 1
+
+
+def test_select_rejects_bad_arguments(lib):
+    st, f = _state(P=16)
+    ws_need = fa.bfasgd_workspace_bytes(16)
+    ws = np.zeros(ws_need + 512, np.uint8)
+    wsp = (ws.ctypes.data + 255) & ~255
+    cnt = np.zeros(2, np.int64)
+    cntp = (cnt.ctypes.data + 7) & ~7
+
+    def sel(c=1.0, eps_c=1e-8, T=0, client=0, cap=16, ws_ptr=wsp, ws_bytes=ws_need, grad=None, s=st):
+        return lib.bfasgd_select_compact(ctypes.byref(s), grad or f.ptr(5), c, eps_c, 7, T, client,
+                                         f.ptr(0), f.ptr(1), cap, cntp, ws_ptr, ws_bytes, None)
+
+    assert sel(c=-1.0) == 2
+    assert sel(c=float("inf")) == 2
+    assert sel(eps_c=float("nan")) == 2
+    assert sel(T=-1) == 2
+    assert sel(T=2 ** 32) == 2
+    assert sel(client=4) == 4
+    assert sel(cap=-1) == 2
+    assert sel(ws_bytes=ws_need - 1) == 6
+    assert sel(ws_ptr=wsp + 8) == 5
+    assert sel(grad=f.ptr(5, misalign=1)) == 5
+    big, f2 = _state(P=2 ** 31)
+    assert sel(s=big) == 2
+
+
+def test_sparse_rejects_bad_arguments(lib):
+    st, f = _state(P=16, T=2)
+    cnt = np.zeros(2, np.int64)
+    cntp = (cnt.ctypes.data + 7) & ~7
+
+    def sp(client=0, ts=0, cap=16, count=cntp):
+        return lib.bfasgd_apply_sparse(ctypes.byref(st), f.ptr(0), f.ptr(1), count, cap, client, ts, None)
+
+    assert sp(ts=3) == 3
+    assert sp(client=9) == 4
+    assert sp(cap=-5) == 2
+    assert sp(count=None) == 1
+    assert sp(count=cntp + 4) == 5
+    assert st.T == 2

@@ -1,0 +1,225 @@
+"""GPU parity of the dense FASGD and SASGD applies against the CPU oracle,
+through the C ABI (workloads: tiny 100k trace, MLP-shaped 1.8M, large 25M)."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1601_04033_amd as fa
+import workload
+from helpers import (RTOL_ONE, RTOL_SEQ, assert_close, assert_state_close, gpu, new_gpu_state,
+                     sample_indices, to_dev)
+
+pytestmark = pytest.mark.gpu
+MODES = [fa.MATH_FAST, fa.MATH_IEEE]
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_tiny_trace_fasgd(mode):
+    """P = 100,000, lambda = 4, 256 updates applied one per call, alpha = 0.01:
+    within 1e-5 after the first update and 1e-4 after all 256."""
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["tiny"]
+    theta0, m, s = workload.host_params(w)
+    clients, ts = workload.schedule(w)
+    st = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, mode)
+    ref = oracle.init_state(theta0, alpha=w.alpha_fasgd)
+    for t in range(w.updates):
+        g = workload.host_gradient(w, m, s, t)
+        fa.fasgd_apply_updates(st, [to_dev(g, dev)], [clients[t]], [ts[t]])
+        oracle.fasgd_apply(ref, g, ts[t])
+        if t == 0:
+            torch.cuda.synchronize()
+            assert_state_close(st, ref, RTOL_ONE, what="after one update")
+    torch.cuda.synchronize()
+    assert_state_close(st, ref, RTOL_SEQ, what="after 256 updates")
+
+
+def test_tiny_trace_sasgd():
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["tiny"]
+    theta0, m, s = workload.host_params(w)
+    clients, ts = workload.schedule(w)
+    st = new_gpu_state(theta0, dev, w.lam, w.alpha_sasgd, fa.MATH_IEEE, sasgd=True)
+    ref = oracle.init_state(theta0, alpha=w.alpha_sasgd)
+    for t in range(w.updates):
+        g = workload.host_gradient(w, m, s, t)
+        fa.sasgd_apply_updates(st, [to_dev(g, dev)], [clients[t]], [ts[t]])
+        oracle.sasgd_apply(ref, g, ts[t])
+        if t == 0:
+            torch.cuda.synchronize()
+            assert_close(st.theta.cpu().numpy(), ref.theta, RTOL_ONE, what="theta after one update")
+    torch.cuda.synchronize()
+    assert_close(st.theta.cpu().numpy(), ref.theta, RTOL_SEQ, what="theta after 256 updates")
+    np.testing.assert_array_equal(st.last_T.cpu().numpy(), ref.last_T)
+    assert st.T == ref.T == w.updates
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_one_client_is_plain_sgd_on_gpu(mode):
+    """One client (tau = 0) with beta = 1, v0 = 1: FASGD on the GPU is SGD."""
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["tiny"]
+    theta0, m, s = workload.host_params(w, 4099)
+    st = new_gpu_state(theta0, dev, 1, 0.01, mode, beta=1.0, v0=1.0)
+    sg = new_gpu_state(theta0, dev, 1, 0.01, mode, sasgd=True)
+    th = torch.from_numpy(theta0).double()
+    for t in range(10):
+        g = workload.host_gradient(w, m, s, t)
+        fa.fasgd_apply_updates(st, [to_dev(g, dev)], [0], [t])
+        fa.sasgd_apply_updates(sg, [to_dev(g, dev)], [0], [t])
+        th -= np.float32(0.01).item() * torch.from_numpy(g).double()
+    torch.cuda.synchronize()
+    assert (st.v.cpu() == 1.0).all()
+    assert_close(st.theta.cpu().numpy(), th.numpy(), RTOL_ONE, what="FASGD theta")
+    assert_close(sg.theta.cpu().numpy(), th.numpy(), RTOL_ONE, what="SASGD theta")
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("K", [2, 3, 7, 8, 9, 16, 33, 64])
+def test_k_fused_equals_sequential(K, mode):
+    """Applying K gradients in one fused pass is bitwise the same as K
+    single-gradient passes (same per-parameter operations, same order);
+    MLP layout, P = 1,796,010 (P mod 4 = 2)."""
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["mlp"]
+    theta0, m, s = workload.host_params(w)
+    clients, ts = workload.schedule(w, K + 40)
+    clients, ts = clients[40:], ts[40:]
+    grads = [to_dev(workload.host_gradient(w, m, s, t), dev) for t in range(K)]
+    fused = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, mode)
+    seq = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, mode)
+    fused.c.T = seq.c.T = 40
+    fa.fasgd_apply_updates(fused, grads, clients, ts)
+    for k in range(K):
+        fa.fasgd_apply_updates(seq, [grads[k]], [clients[k]], [ts[k]])
+    torch.cuda.synchronize()
+    for name in ("theta", "n", "b", "v", "last_T"):
+        assert torch.equal(getattr(fused, name), getattr(seq, name)), name
+    assert fused.T == seq.T == 40 + K
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_mlp_fasgd_k16_sampled(mode):
+    """MLP-shaped workload, P = 1,796,010, lambda = 16, 2,000 updates in
+    passes of K = 16, Poisson(lambda - 1) staleness; the oracle follows a
+    sample of parameters (every update is elementwise)."""
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["mlp"]
+    theta0, m, s = workload.host_params(w)
+    clients, ts = workload.schedule(w)
+    js = sample_indices(w.P, 3000)
+    jt = torch.from_numpy(js).to(dev)
+    dm, ds = to_dev(m, dev), to_dev(s, dev)
+    st = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, mode)
+    ref = oracle.init_state(theta0[js], alpha=w.alpha_fasgd)
+    K = 16
+    bufs = [torch.empty(w.P, device=dev) for _ in range(K)]
+    for p in range(w.updates // K):
+        for k in range(K):
+            workload.device_gradient(w, dm, ds, p * K + k, out=bufs[k])
+        sl = slice(p * K, (p + 1) * K)
+        fa.fasgd_apply_updates(st, bufs, clients[sl], ts[sl])
+        samples = [b_[jt].cpu().numpy() for b_ in bufs]
+        for k in range(K):
+            oracle.fasgd_apply(ref, samples[k], ts[p * K + k])
+        if p == 0:
+            torch.cuda.synchronize()
+            assert_state_close(st, ref, RTOL_ONE, js=jt, what="after the first pass")
+    torch.cuda.synchronize()
+    assert_state_close(st, ref, RTOL_SEQ, js=jt, what="after 2000 updates")
+
+
+@pytest.mark.parametrize("K", [1, 8, 32])
+def test_large_25m_sampled(K):
+    """P = 25,000,000 in 50 blocks of 500k, lambda = 64, uniform 0..2 lambda
+    delays; 64 updates in passes of K (FAST mode, the benchmarked one)."""
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["large"]
+    theta0, m, s = workload.device_params(w, dev)
+    clients, ts = workload.schedule(w, 64)
+    js = sample_indices(w.P, 4096)
+    jt = torch.from_numpy(js).to(dev)
+    st = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, fa.MATH_FAST)
+    ref = oracle.init_state(theta0[jt].cpu().numpy(), alpha=w.alpha_fasgd)
+    bufs = [torch.empty(w.P, device=dev) for _ in range(K)]
+    for p in range(64 // K):
+        for k in range(K):
+            workload.device_gradient(w, m, s, p * K + k, out=bufs[k])
+        sl = slice(p * K, (p + 1) * K)
+        fa.fasgd_apply_updates(st, bufs, clients[sl], ts[sl])
+        for k in range(K):
+            oracle.fasgd_apply(ref, bufs[k][jt].cpu().numpy(), ts[p * K + k])
+        if p == 0:
+            torch.cuda.synchronize()
+            assert_state_close(st, ref, RTOL_ONE if K == 1 else RTOL_SEQ, js=jt, what="first pass")
+    torch.cuda.synchronize()
+    assert_state_close(st, ref, RTOL_SEQ, js=jt, what="after 64 updates")
+    del bufs
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("P", [1, 2, 3, 4, 5, 6, 7, 8, 9, 4095, 4097, 1023 * 256 + 3])
+@pytest.mark.parametrize("mode", MODES)
+def test_small_and_ragged_sizes(P, mode):
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["tiny"]
+    theta0, m, s = workload.host_params(w, P, seed=P)
+    clients, ts = workload.schedule(w, 12)
+    st = new_gpu_state(theta0, dev, w.lam, 0.01, mode)
+    ref = oracle.init_state(theta0, alpha=0.01)
+    grads = [workload.host_gradient(w, m, s, t, seed=P) for t in range(12)]
+    fa.fasgd_apply_updates(st, [to_dev(g, dev) for g in grads[:5]], clients[:5], ts[:5])
+    fa.fasgd_apply_updates(st, [to_dev(g, dev) for g in grads[5:]], clients[5:], ts[5:])
+    for t in range(12):
+        oracle.fasgd_apply(ref, grads[t], ts[t])
+    torch.cuda.synchronize()
+    assert_state_close(st, ref, RTOL_SEQ, what=f"P={P}")
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_misaligned_views_use_scalar_path(mode):
+    """Arrays offset by one element (4-byte aligned only) give the same result."""
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["tiny"]
+    P = 10_001
+    theta0, m, s = workload.host_params(w, P, seed=9)
+    clients, ts = workload.schedule(w, 6)
+    big = [torch.empty(P + 1, device=dev) for _ in range(4)]
+    lt = torch.empty(P + 1, device=dev, dtype=torch.int32)
+    theta, n, b, v, last_T = big[0][1:], big[1][1:], big[2][1:], big[3][1:], lt[1:]
+    theta.copy_(torch.from_numpy(theta0))
+    st = fa.fasgd_init_state(theta, n, b, v, last_T, lam=w.lam, alpha=0.01, math_mode=mode)
+    gb = [torch.empty(P + 1, device=dev) for _ in range(6)]
+    grads = [workload.host_gradient(w, m, s, t, seed=9) for t in range(6)]
+    for k in range(6):
+        gb[k][1:].copy_(torch.from_numpy(grads[k]))
+    fa.fasgd_apply_updates(st, [g[1:] for g in gb], clients, ts)
+    ref = oracle.init_state(theta0, alpha=0.01)
+    for t in range(6):
+        oracle.fasgd_apply(ref, grads[t], ts[t])
+    torch.cuda.synchronize()
+    assert_state_close(st, ref, RTOL_SEQ, what="misaligned")
+
+
+def test_rejected_call_changes_nothing():
+    import torch
+    dev = gpu()
+    P = 1000
+    st = new_gpu_state(np.ones(P, np.float32), dev, 2, 0.01, fa.MATH_FAST)
+    g = torch.ones(P, device=dev)
+    with pytest.raises(fa.FasgdError) as e:
+        fa.fasgd_apply_updates(st, [g, g], [0, 1], [0, 2])      # second: ts 2 > T + 1
+    assert e.value.status == 3
+    with pytest.raises(fa.FasgdError) as e:
+        fa.fasgd_apply_updates(st, [g], [2], [0])               # client 2 >= lambda
+    assert e.value.status == 4
+    torch.cuda.synchronize()
+    assert st.T == 0 and (st.theta.cpu() == 1.0).all() and (st.last_T.cpu() == -1).all()

@@ -1,0 +1,174 @@
+"""Full-size GPU checks on sampled outputs: the 1e9-parameter step in the
+launch configuration the benchmark times (K = 32 fused FASGD pass, then one
+B-FASGD push selected at about 10 % and applied sparsely), and the largest
+sizes the ABI accepts."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1601_04033_amd as fa
+import workload
+from helpers import RTOL_SEQ, assert_close, assert_state_close, gpu, new_gpu_state, sample_indices
+
+pytestmark = pytest.mark.gpu
+SEED = 0x5EED
+
+
+def _free():
+    import gc
+    import torch
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def _calibrate_c(v, target):
+    vd = np.asarray(v, np.float64) + 1e-8
+    lo, hi = 0.0, 1e7
+    for _ in range(100):
+        c = 0.5 * (lo + hi)
+        lo, hi = (c, hi) if (vd / (vd + c)).mean() > target else (lo, c)
+    return oracle.f32(c)
+
+
+def _philox_r(js, seed, T, client):
+    out = np.empty(len(js))
+    for i, j in enumerate(js):
+        j = int(j)
+        q = j >> 2
+        w = oracle.philox4x32_10([q & 0xFFFFFFFF, q >> 32, T & 0xFFFFFFFF, client],
+                                 [seed & 0xFFFFFFFF, seed >> 32])[j & 3]
+        out[i] = (int(w) >> 8) * 2.0 ** -24
+    return out
+
+
+def test_memscale_1e9_step_sampled():
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["memscale"]
+    P, K = w.P, 32
+    free, total = torch.cuda.mem_get_info()
+    if free < 170e9:
+        pytest.skip(f"needs about 170 GB of free device memory, {free / 1e9:.0f} GB free")
+    print(f"memscale: P={P} K={K}", flush=True)
+    theta0, m, s = workload.device_params(w, dev)
+    clients, ts = workload.schedule(w, K + 1)
+    js = sample_indices(P, 4096, seed=1)
+    jt = torch.from_numpy(js).to(dev)
+    st = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, fa.MATH_FAST)
+    ref = oracle.init_state(theta0[jt].cpu().numpy(), alpha=w.alpha_fasgd)
+    del theta0
+    grads = [workload.device_gradient(w, m, s, t) for t in range(K + 1)]
+    del m, s
+    fa.fasgd_apply_updates(st, grads[:K], clients[:K], ts[:K])
+    for k in range(K):
+        oracle.fasgd_apply(ref, grads[k][jt].cpu().numpy(), ts[k])
+    torch.cuda.synchronize()
+    assert_state_close(st, ref, RTOL_SEQ, js=jt, what="after the K = 32 pass")
+
+    c = _calibrate_c(ref.v, w.transmit_fraction)
+    cap = P // 4
+    idx = torch.empty(cap, device=dev, dtype=torch.int32)
+    val = torch.empty(cap, device=dev)
+    cnt = torch.zeros(1, device=dev, dtype=torch.int64)
+    ws = fa.allocate_workspace(P, dev)
+    gK = grads[K]
+    fa.bfasgd_select_compact(st, gK, c, 1e-8, SEED, st.T, clients[K], idx, val, cnt, ws)
+    torch.cuda.synchronize()
+    mm = int(cnt.item())
+    assert 0.08 < mm / P < 0.12, mm / P
+    lst = idx[:mm]
+    assert bool((lst[1:] > lst[:-1]).all())                     # strictly ascending
+    assert torch.equal(gK[lst.long()].view(torch.int32), val[:mm].view(torch.int32))
+    pos = torch.searchsorted(lst, jt.to(torch.int32))
+    got = ((pos < mm) & (lst[pos.clamp(max=mm - 1)] == jt.to(torch.int32))).cpu().numpy()
+    v32 = ref.v.astype(np.float32)
+    want = oracle.bfasgd_decide(js, v32, c, 1e-8, SEED, ref.T, clients[K])
+    diff = got != want
+    if diff.any():     # only near-ties of the fp32 v drift may differ
+        tv = v32[diff].astype(np.float64) + 1e-8
+        p = tv / (tv + c)
+        assert (np.abs(_philox_r(js[diff], SEED, ref.T, int(clients[K])) - p) <= 2 * RTOL_SEQ * p).all()
+        assert diff.sum() <= 4
+    g_at = gK[jt].cpu().numpy()
+    sel = np.flatnonzero(want & ~diff)
+    fa.bfasgd_apply_sparse(st, idx, val, cnt, clients[K], ts[K])
+    oracle.bfasgd_apply_sparse(ref, sel.astype(np.int32), g_at[sel], ts[K])
+    torch.cuda.synchronize()
+    keep = np.flatnonzero(~diff)
+    assert_state_close(st, ref.take(keep), RTOL_SEQ, js=torch.from_numpy(js[keep]).to(dev),
+                       what="after the B-FASGD push")
+    del grads, gK, st, idx, val, ws, lst
+    _free()
+
+
+def test_select_at_int32_index_limit():
+    """P = 2^31 - 1, the largest B-FASGD size (int32 indices)."""
+    import torch
+    dev = gpu()
+    P = 2 ** 31 - 1
+    free, _ = torch.cuda.mem_get_info()
+    if free < 40e9:
+        pytest.skip("needs about 40 GB of free device memory")
+    print(f"select: P={P}", flush=True)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(77)
+    v = torch.exp(torch.rand(P, device=dev, generator=gen) * 5.0)          # v in [1, e^5]
+    g = torch.randn(P, device=dev, generator=gen)
+    st = fa.fasgd_init_state(torch.empty(1, device=dev), None, None, None,
+                             torch.empty(1, device=dev, dtype=torch.int32), lam=4, alpha=0.01)
+    st.c.P = P
+    st.c.v = v.data_ptr()
+    st.tensors["v"] = v
+    idx = torch.empty(P, device=dev, dtype=torch.int32)
+    val = torch.empty(P, device=dev)
+    cnt = torch.zeros(1, device=dev, dtype=torch.int64)
+    ws = fa.allocate_workspace(P, dev)
+    c = 300.0
+    fa.bfasgd_select_compact(st, g, c, 1e-8, SEED, 3, 1, idx, val, cnt, ws)
+    torch.cuda.synchronize()
+    mm = int(cnt.item())
+    js = np.unique(np.concatenate([np.arange(P - 4096, P), sample_indices(P, 4096, seed=2)]))
+    jt = torch.from_numpy(js).to(dev)
+    want = oracle.bfasgd_decide(js, v[jt].cpu().numpy(), c, 1e-8, SEED, 3, 1)
+    lst = idx[:mm]
+    pos = torch.searchsorted(lst, jt.to(torch.int32))
+    got = ((pos < mm) & (lst[pos.clamp(max=mm - 1)] == jt.to(torch.int32))).cpu().numpy()
+    np.testing.assert_array_equal(got, want)
+    assert bool((lst[1:] > lst[:-1]).all())
+    assert torch.equal(g[lst.long()].view(torch.int32), val[:mm].view(torch.int32))
+    # the tail of the list is exactly the oracle's transmitted indices of the last 4096
+    in_tail = js >= P - 4096
+    np.testing.assert_array_equal(lst[lst >= P - 4096].cpu().numpy(), js[in_tail & want])
+    vs = v[jt].double().cpu().numpy() + 1e-8
+    assert abs(mm / P - (vs / (vs + c)).mean()) < 0.01
+    del v, g, idx, val, ws, lst
+    _free()
+
+
+def test_dense_beyond_int32_parameters():
+    """P = 2^31 + 5: 64-bit offsets in the dense kernels and the ragged tail."""
+    import torch
+    dev = gpu()
+    P = 2 ** 31 + 5
+    free, _ = torch.cuda.mem_get_info()
+    if free < 75e9:
+        pytest.skip("needs about 75 GB of free device memory")
+    print(f"dense: P={P}", flush=True)
+    w = workload.WORKLOADS["memscale"]
+    theta0, m, s = workload.device_params(w, dev, P=P)
+    js = np.unique(np.concatenate([np.arange(P - 70, P), sample_indices(P, 2048, seed=3)]))
+    jt = torch.from_numpy(js).to(dev)
+    st = new_gpu_state(theta0, dev, 8, 0.005, fa.MATH_FAST)
+    ref = oracle.init_state(theta0[jt].cpu().numpy(), alpha=0.005)
+    del theta0
+    grads = [workload.device_gradient(w, m, s, t) for t in range(2)]
+    fa.fasgd_apply_updates(st, grads, [0, 1], [0, 0])
+    for k in range(2):
+        oracle.fasgd_apply(ref, grads[k][jt].cpu().numpy(), 0)
+    sg = [grads[0]]
+    fa.sasgd_apply_updates(st, sg, [2], [1])
+    oracle.sasgd_apply(ref, grads[0][jt].cpu().numpy(), 1)
+    torch.cuda.synchronize()
+    assert_state_close(st, ref, RTOL_SEQ, js=jt, what="P > 2^31")
+    del grads, sg, st, m, s
+    _free()
