@@ -185,7 +185,7 @@ def main():
     updates = steps * P * K + sum(m_list)
     value = updates / wall
     dense_ms = float(np.mean(ms["dense"]))
-    dense_bytes = P * (36 + 4 * K)          # per launch: state 16 B read + 16 B write + 4 B last_T, 4 B per gradient
+    dense_bytes = P * (32 + 4 * K)          # per launch: state 16 B read + 16 B write, 4 B per gradient
     achieved = dense_bytes / (dense_ms * 1e-3) / 1e9
     traffic = measured_traffic(P, K)
     sel_ms, sp_ms = float(np.mean(ms["select"])), float(np.mean(ms["sparse"]))
@@ -203,7 +203,22 @@ def main():
         torch.cuda.synchronize()
         sas_ms.append(a.elapsed_time(b_))
     sas_ms_avg = float(np.mean(sas_ms[1:]))
-    sas_bytes = P * (12 + 4 * K)
+    sas_bytes = P * (8 + 4 * K)
+
+    # plain copy of one gradient buffer (4P bytes read, 4P written): the
+    # bandwidth anchor, and the known-size kernel that calibrates the
+    # rocprofv3 FETCH_SIZE / WRITE_SIZE counters
+    anchor = torch.empty_like(pool[0])
+    cp_ms = []
+    for r in range(3):
+        a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        anchor.copy_(pool[r % K])
+        b_.record()
+        torch.cuda.synchronize()
+        cp_ms.append(a.elapsed_time(b_))
+    copy_gbs = 8 * P / (float(np.mean(cp_ms[1:])) * 1e-3) / 1e9
+    del anchor
 
     out = {
         "metric": METRIC,
@@ -231,6 +246,7 @@ def main():
                                       "transmitted_fraction": m_avg / P},
             "bfasgd_apply_sparse": {"ms": sp_ms, "GB/s_algorithmic": sp_bytes / (sp_ms * 1e-3) / 1e9},
             "sasgd_apply_updates": {"ms": sas_ms_avg, "GB/s": sas_bytes / (sas_ms_avg * 1e-3) / 1e9},
+            "copy_anchor": {"GB/s": copy_gbs, "bytes": 8 * P},
         },
     }
     if args.cpu_params:

@@ -61,11 +61,16 @@ typedef enum fasgd_math {
  *   n       moving average of the squared gradient, fp32 [P]
  *   b       moving average of the gradient, fp32 [P]
  *   v       moving average of 1/sqrt(n - b^2 + eps), fp32 [P]
- *   last_T  timestamp of the last update that touched each parameter,
- *           int32 [P], -1 before the first
+ *   last_T  timestamp of the last sparse (B-FASGD) update of each
+ *           parameter, int32 [P], -1 before the first
+ * Per-parameter staleness bookkeeping: a dense apply updates every
+ * parameter, so it records its timestamp once in dense_T instead of
+ * writing P copies of it; the last update that touched parameter j is
+ * max(last_T[j], dense_T) (-1: never updated).
  * Hyper-parameters: alpha (Sec. 2.1), gamma, beta, eps (Sec. 2.2).
  * lambda bounds the client ids; mu is recorded only (a gradient arrives as
- * the minibatch mean, Sec. 2.2).  T is advanced by the apply calls.
+ * the minibatch mean, Sec. 2.2).  T and dense_T are advanced by the apply
+ * calls.
  */
 typedef struct fasgd_state {
     int64_t P;
@@ -78,6 +83,7 @@ typedef struct fasgd_state {
     int32_t math_mode;          /* fasgd_math */
     int32_t reserved;           /* 0 */
     int64_t T;
+    int64_t dense_T;            /* timestamp of the last dense update, -1 before the first */
     float* theta;
     float* n;
     float* b;
@@ -88,8 +94,8 @@ typedef struct fasgd_state {
 /*
  * Initialise a server (the FRED Server initialisation function, Sec. 3):
  * fills n, b and v with n0, b0, v0 and last_T with -1 on `stream`, sets
- * T = 0 (Sec. 2.1) and records the hyper-parameters in *st.  theta must
- * already hold the initial parameters; it is not written.
+ * T = 0 (Sec. 2.1) and dense_T = -1, and records the hyper-parameters in
+ * *st.  theta must already hold the initial parameters; it is not written.
  * Requires P >= 1, lambda >= 1, mu >= 1, alpha > 0, gamma and beta in
  * [0, 1], eps > 0 (finite), math_mode a fasgd_math value.
  * n, b, v may be NULL for a state used only with sasgd_apply_updates.
@@ -109,13 +115,15 @@ fasgd_status fasgd_init_state(fasgd_state* st, int64_t P, int32_t lambda, int32_
  *   theta <- theta - alpha / (v max(tau_k, 1)) g,
  * one gradient after the other (the server lock serialises arrivals,
  * Sec. 2.1), with each parameter's state held in registers across the K
- * gradients.  last_T becomes T + K - 1 and T advances by K.
+ * gradients.  dense_T becomes T + K - 1 and T advances by K; last_T is not
+ * touched.
  *   grads    host array of K device pointers, each fp32 [P]
  *   clients  host int32 [K], each in [0, lambda)
  *   grad_ts  host int64 [K], 0 <= grad_ts[k] <= T + k
  *   K        1 .. FASGD_MAX_K
  * Errors: FASGD_ERR_STALENESS if some grad_ts[k] > T + k; FASGD_ERR_ARG if
- * K is out of range or T + K - 1 exceeds INT32_MAX (last_T is int32).
+ * K is out of range or T + K - 1 exceeds INT32_MAX (timestamps are kept
+ * within the int32 range of last_T).
  */
 fasgd_status fasgd_apply_updates(fasgd_state* st, const float* const* grads, const int32_t* clients,
                                  const int64_t* grad_ts, int32_t K, hipStream_t stream);
@@ -123,8 +131,8 @@ fasgd_status fasgd_apply_updates(fasgd_state* st, const float* const* grads, con
 /*
  * SASGD apply-update (staleness-aware ASGD, Sec. 1 and 2.1): the rate of
  * the k-th gradient is alpha / max(tau_k, 1), theta <- theta - that * g.
- * Reads and writes theta and last_T only (n, b, v may be NULL).  Same
- * arguments, order and errors as fasgd_apply_updates.
+ * Reads and writes theta only (n, b, v may be NULL) and sets dense_T as
+ * fasgd_apply_updates does.  Same arguments, order and errors.
  */
 fasgd_status sasgd_apply_updates(fasgd_state* st, const float* const* grads, const int32_t* clients,
                                  const int64_t* grad_ts, int32_t K, hipStream_t stream);

@@ -44,7 +44,7 @@ class fasgd_state(ctypes.Structure):
     _fields_ = [("P", ctypes.c_int64), ("lambda_", ctypes.c_int32), ("mu", ctypes.c_int32),
                 ("alpha", ctypes.c_float), ("gamma", ctypes.c_float), ("beta", ctypes.c_float),
                 ("eps", ctypes.c_float), ("math_mode", ctypes.c_int32), ("reserved", ctypes.c_int32),
-                ("T", ctypes.c_int64),
+                ("T", ctypes.c_int64), ("dense_T", ctypes.c_int64),
                 ("theta", ctypes.c_void_p), ("n", ctypes.c_void_p), ("b", ctypes.c_void_p),
                 ("v", ctypes.c_void_p), ("last_T", ctypes.c_void_p)]
 
@@ -121,6 +121,16 @@ class State:
     @property
     def P(self) -> int:
         return int(self.c.P)
+
+    @property
+    def dense_T(self) -> int:
+        return int(self.c.dense_T)
+
+    def last_update(self):
+        """Device int32 [P]: timestamp of the last update of each parameter,
+        max(last_T, dense_T) (-1: never updated)."""
+        import torch
+        return torch.clamp(self.tensors["last_T"], min=int(self.c.dense_T))
 
     def __getattr__(self, name):
         t = self.__dict__.get("tensors", {})

@@ -42,6 +42,8 @@ fasgd_status check_state(const fasgd_state* st, bool need_stats)
     if (st->P < 1) return fail(FASGD_ERR_ARG, "P = %lld must be >= 1", (long long)st->P);
     if (st->lambda < 1) return fail(FASGD_ERR_ARG, "lambda = %d must be >= 1", st->lambda);
     if (st->T < 0 || st->T > INT32_MAX) return fail(FASGD_ERR_ARG, "T = %lld out of range", (long long)st->T);
+    if (st->dense_T < -1 || st->dense_T >= st->T)
+        return fail(FASGD_ERR_ARG, "dense_T = %lld is not in [-1, T)", (long long)st->dense_T);
     if (!st->theta || !st->last_T) return fail(FASGD_ERR_NULL, "theta or last_T is NULL");
     if (need_stats && (!st->n || !st->b || !st->v)) return fail(FASGD_ERR_NULL, "n, b or v is NULL");
     if (!aligned(st->theta, 4) || !aligned(st->last_T, 4) || (st->n && !aligned(st->n, 4)) ||
@@ -88,11 +90,11 @@ fasgd_status dense_common(fasgd_state* st, const float* const* grads, const int3
     if (s != FASGD_OK) return s;
     if (!grads || !clients || !grad_ts) return fail(FASGD_ERR_NULL, "grads, clients or grad_ts is NULL");
     if (K < 1 || K > FASGD_MAX_K) return fail(FASGD_ERR_ARG, "K = %d is not in [1, %d]", K, FASGD_MAX_K);
-    if (st->T + K - 1 > INT32_MAX) return fail(FASGD_ERR_ARG, "T + K - 1 exceeds the int32 last_T range");
+    if (st->T + K - 1 > INT32_MAX) return fail(FASGD_ERR_ARG, "T + K - 1 exceeds the int32 timestamp range");
     float tau_div[FASGD_MAX_K];
     s = staleness(st, clients, grad_ts, K, tau_div);
     if (s != FASGD_OK) return s;
-    vec = aligned(st->theta, 16) && aligned(st->last_T, 16) &&
+    vec = aligned(st->theta, 16) &&
           (!fasgd_mode || (aligned(st->n, 16) && aligned(st->b, 16) && aligned(st->v, 16)));
     memset(&a, 0, sizeof a);
     for (int32_t k = 0; k < K; ++k) {
@@ -107,10 +109,8 @@ fasgd_status dense_common(fasgd_state* st, const float* const* grads, const int3
     a.n = st->n;
     a.b = st->b;
     a.v = st->v;
-    a.last_T = st->last_T;
     a.P = st->P;
     a.K = K;
-    a.last_T_value = static_cast<int32_t>(st->T + K - 1);
     a.h = hyper_of(st);
     return FASGD_OK;
 }
@@ -153,6 +153,7 @@ fasgd_status fasgd_init_state(fasgd_state* st, int64_t P, int32_t lambda, int32_
     s.eps = eps;
     s.math_mode = math_mode;
     s.T = 0;
+    s.dense_T = -1;
     s.theta = theta;
     s.n = n;
     s.b = b;
@@ -171,6 +172,7 @@ fasgd_status fasgd_apply_updates(fasgd_state* st, const float* const* grads, con
     if (s != FASGD_OK) return s;
     const hipError_t e = fasgd::launch_fasgd_dense(a, st->math_mode, vec, stream);
     if (e != hipSuccess) return hip_fail(e, "fasgd_apply_updates");
+    st->dense_T = st->T + K - 1;
     st->T += K;
     return ok();
 }
@@ -184,6 +186,7 @@ fasgd_status sasgd_apply_updates(fasgd_state* st, const float* const* grads, con
     if (s != FASGD_OK) return s;
     const hipError_t e = fasgd::launch_sasgd_dense(a, vec, stream);
     if (e != hipSuccess) return hip_fail(e, "sasgd_apply_updates");
+    st->dense_T = st->T + K - 1;
     st->T += K;
     return ok();
 }

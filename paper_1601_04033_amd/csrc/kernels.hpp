@@ -18,12 +18,10 @@ struct DenseArgs {
     float* n;
     float* b;
     float* v;
-    int32_t* last_T;
     const float* grad[kMaxK];
     float coef[kMaxK];      // FASGD IEEE: tau_k; FASGD FAST and SASGD: alpha / tau_k
     int64_t P;
     int32_t K;
-    int32_t last_T_value;   // T + K - 1
     Hyper h;
 };
 

@@ -46,9 +46,9 @@ def assert_state_close(st_gpu, ref, rtol, js=None, what=""):
         t = st_gpu.tensors[name]
         got = (t[js] if js is not None else t).cpu().numpy()
         assert_close(got, getattr(ref, name), rtol, ATOL, f"{what} {name}")
-    lt = st_gpu.tensors["last_T"]
+    lt = st_gpu.last_update()            # max(last_T, dense_T)
     got = (lt[js] if js is not None else lt).cpu().numpy()
-    np.testing.assert_array_equal(got.astype(np.int64), ref.last_T, err_msg=f"{what} last_T")
+    np.testing.assert_array_equal(got.astype(np.int64), ref.last_T, err_msg=f"{what} last update")
     assert st_gpu.T == ref.T
 
 

@@ -71,7 +71,7 @@ def _state(P=16, lam=4, T=0):
     st = fa.fasgd_state()
     st.P, st.lambda_, st.mu = P, lam, 1
     st.alpha, st.gamma, st.beta, st.eps = 0.01, 0.95, 0.9, 1e-4
-    st.math_mode, st.T = 1, T
+    st.math_mode, st.T, st.dense_T = 1, T, -1
     st.theta, st.n, st.b, st.v, st.last_T = f.ptr(0), f.ptr(1), f.ptr(2), f.ptr(3), f.ptr(4)
     return st, f
 
@@ -108,7 +108,13 @@ def test_dense_rejects_bad_arguments(lib, fn):
     mis, f3 = _state()
     mis.theta = f3.ptr(0, misalign=2)
     assert _call_dense(lib, fn, mis, [0], fake=f3) == 5
-    # last_T is int32: T + K - 1 must fit
+    # dense_T must lie in [-1, T)
+    dt, f5 = _state(T=3)
+    dt.dense_T = 3
+    assert _call_dense(lib, fn, dt, [0], fake=f5) == 2
+    dt.dense_T = -2
+    assert _call_dense(lib, fn, dt, [0], fake=f5) == 2
+    # timestamps stay in the int32 range of last_T: T + K - 1 must fit
     big, f4 = _state(T=2 ** 31 - 2)
     assert _call_dense(lib, fn, big, [0, 0, 0], fake=f4) == 2
     # nothing was applied

@@ -142,8 +142,10 @@ def test_sparse_apply_matches_oracle_and_transmit_all_is_dense(mode):
         fa.bfasgd_apply_sparse(sparse, idx, val, cnt, clients[t], ts[t])
     torch.cuda.synchronize()
     assert int(cnt.item()) == P
-    for name in ("theta", "n", "b", "v", "last_T"):
+    for name in ("theta", "n", "b", "v"):
         assert torch.equal(getattr(dense, name), getattr(sparse, name)), name
+    assert torch.equal(dense.last_update(), sparse.last_update())
+    assert (dense.last_T.cpu() == -1).all() and dense.dense_T == 7 and sparse.dense_T == -1
 
 
 @pytest.mark.parametrize("mode", [fa.MATH_FAST, fa.MATH_IEEE])

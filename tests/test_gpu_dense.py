@@ -52,7 +52,8 @@ def test_tiny_trace_sasgd():
             assert_close(st.theta.cpu().numpy(), ref.theta, RTOL_ONE, what="theta after one update")
     torch.cuda.synchronize()
     assert_close(st.theta.cpu().numpy(), ref.theta, RTOL_SEQ, what="theta after 256 updates")
-    np.testing.assert_array_equal(st.last_T.cpu().numpy(), ref.last_T)
+    np.testing.assert_array_equal(st.last_update().cpu().numpy(), ref.last_T)
+    assert (st.last_T.cpu() == -1).all() and st.dense_T == w.updates - 1
     assert st.T == ref.T == w.updates
 
 
@@ -99,7 +100,7 @@ def test_k_fused_equals_sequential(K, mode):
     torch.cuda.synchronize()
     for name in ("theta", "n", "b", "v", "last_T"):
         assert torch.equal(getattr(fused, name), getattr(seq, name)), name
-    assert fused.T == seq.T == 40 + K
+    assert fused.T == seq.T == 40 + K and fused.dense_T == seq.dense_T == 40 + K - 1
 
 
 @pytest.mark.parametrize("mode", MODES)
@@ -222,4 +223,5 @@ def test_rejected_call_changes_nothing():
         fa.fasgd_apply_updates(st, [g], [2], [0])               # client 2 >= lambda
     assert e.value.status == 4
     torch.cuda.synchronize()
-    assert st.T == 0 and (st.theta.cpu() == 1.0).all() and (st.last_T.cpu() == -1).all()
+    assert st.T == 0 and st.dense_T == -1
+    assert (st.theta.cpu() == 1.0).all() and (st.last_T.cpu() == -1).all()
