@@ -40,7 +40,9 @@ struct SelectArgs {
     int64_t* d_count;
     uint64_t* ballots;      // 4 per 64 chunks of 4 parameters
     uint32_t* tile_count;
-    uint32_t* tile_offset;
+    uint32_t* tile_offset;   // within its group of 1024 tiles
+    uint32_t* group_total;
+    uint32_t* group_offset;
     int64_t P;
     int64_t capacity;
     int64_t n_tiles;
