@@ -45,6 +45,10 @@ def _load():
     lib.oracle_bfasgd_select.restype = ctypes.c_int64
     lib.oracle_bfasgd_apply_sparse.argtypes = [dp, dp, dp, dp, i64p, i64p, i32p, fp, i64, i64, d, d, d, d]
     lib.oracle_bfasgd_apply_sparse.restype = ctypes.c_int
+    lib.oracle_sync_sgd_apply.argtypes = [i64, dp, i64p, i64p, P(fp), i32, d]
+    lib.oracle_sync_sgd_apply.restype = None
+    lib.oracle_bfasgd_apply_cached.argtypes = [i64, dp, dp, dp, dp, i64p, i64p, fp, i32p, fp, i64, i64, d, d, d, d]
+    lib.oracle_bfasgd_apply_cached.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -196,6 +200,48 @@ def bfasgd_apply_sparse(st: State, idx, val, grad_ts: int) -> None:
                                         _ptr(st.last_T, ctypes.c_int64), ctypes.byref(T),
                                         _ptr(idx, ctypes.c_int32), _ptr(val, ctypes.c_float), idx.shape[0],
                                         int(grad_ts), h["alpha"], h["gamma"], h["beta"], h["eps"])
+    if rc != 0:
+        raise OracleError(f"negative staleness: grad_ts={grad_ts} > T={st.T}")
+    st.T = T.value
+
+
+def sync_sgd_apply(st: State, grads, lr) -> None:
+    """Synchronous SGD step (Sec. 3 listing): every one of the lambda
+    gradients applied as theta -= lr * (g / lambda) in client order; T += 1."""
+    lib = _load()
+    gs = [np.ascontiguousarray(g, dtype=np.float32) for g in grads]
+    for g in gs:
+        if g.shape != (st.P,):
+            raise OracleError("gradient length differs from P")
+    arr = (ctypes.POINTER(ctypes.c_float) * len(gs))(*[_ptr(g, ctypes.c_float) for g in gs])
+    T = ctypes.c_int64(st.T)
+    lib.oracle_sync_sgd_apply(st.P, _ptr(st.theta, ctypes.c_double), _ptr(st.last_T, ctypes.c_int64),
+                              ctypes.byref(T), arr, len(gs), f32(lr))
+    st.T = T.value
+
+
+def bfasgd_apply_cached(st: State, cache, idx, val, grad_ts: int) -> None:
+    """Push with dropped values re-applied from the client's cache (Sec. 2.3):
+    cache[idx] = val, then a FASGD update with the whole cache.  cache
+    (float32 [P]) is updated in place."""
+    lib = _load()
+    _check(cache, np.float32, "cache")
+    if cache.shape != (st.P,):
+        raise OracleError("cache length differs from P")
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    val = np.ascontiguousarray(val, dtype=np.float32)
+    if idx.shape != val.shape:
+        raise OracleError("idx and val differ in shape")
+    if idx.size and (idx.min() < 0 or idx.max() >= st.P):
+        raise OracleError("index out of range")
+    T = ctypes.c_int64(st.T)
+    h = st.hyper
+    rc = lib.oracle_bfasgd_apply_cached(st.P, _ptr(st.theta, ctypes.c_double), _ptr(st.n, ctypes.c_double),
+                                        _ptr(st.b, ctypes.c_double), _ptr(st.v, ctypes.c_double),
+                                        _ptr(st.last_T, ctypes.c_int64), ctypes.byref(T),
+                                        _ptr(cache, ctypes.c_float), _ptr(idx, ctypes.c_int32),
+                                        _ptr(val, ctypes.c_float), idx.shape[0], int(grad_ts),
+                                        h["alpha"], h["gamma"], h["beta"], h["eps"])
     if rc != 0:
         raise OracleError(f"negative staleness: grad_ts={grad_ts} > T={st.T}")
     st.T = T.value

@@ -214,3 +214,40 @@ int oracle_bfasgd_apply_sparse(double *theta, double *n, double *b, double *v, i
     *T += 1;
     return 0;
 }
+
+/* ------------------------------------------------------------------------- */
+/* Synchronous SGD server (the apply-update listing of Sec. 3): once all      */
+/* lambda clients have pushed, every gradient is applied in client order as   */
+/* p <- p - lr * (g / lambda); the timestamp then advances by one.            */
+/* ------------------------------------------------------------------------- */
+void oracle_sync_sgd_apply(int64_t P, double *theta, int64_t *last_T, int64_t *T,
+                           const float *const *grads, int32_t lambda, double lr)
+{
+    for (int32_t k = 0; k < lambda; ++k) {
+        for (int64_t j = 0; j < P; ++j) {
+            double mod = (double)grads[k][j] / (double)lambda;
+            theta[j] = theta[j] - lr * mod;
+        }
+    }
+    if (last_T)
+        for (int64_t j = 0; j < P; ++j)
+            last_T[j] = *T;
+    *T += 1;
+}
+
+/*
+ * Dropped pushes re-apply the client's most recent gradient (Sec. 2.3),
+ * per parameter: cache holds, for one client, the last value it transmitted
+ * for each parameter (0 before the first).  The transmitted (index, value)
+ * pairs overwrite the cache, and the whole cache is then applied as one
+ * FASGD gradient (Sec. 2.2).
+ */
+int oracle_bfasgd_apply_cached(int64_t P, double *theta, double *n, double *b, double *v,
+                               int64_t *last_T, int64_t *T, float *cache, const int32_t *idx,
+                               const float *val, int64_t m, int64_t grad_ts, double alpha,
+                               double gamma, double beta, double eps)
+{
+    for (int64_t i = 0; i < m; ++i)
+        cache[idx[i]] = val[i];
+    return oracle_fasgd_apply(P, theta, n, b, v, last_T, T, cache, grad_ts, alpha, gamma, beta, eps);
+}
