@@ -205,6 +205,34 @@ def main():
     sas_ms_avg = float(np.mean(sas_ms[1:]))
     sas_bytes = P * (8 + 4 * K)
 
+    def timed(fn, reps=3):
+        out = []
+        for _ in range(reps):
+            a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b_.record()
+            torch.cuda.synchronize()
+            out.append(a.elapsed_time(b_))
+        return float(np.mean(out[1:]))
+
+    # widened paths at the same shape, after the timed region
+    #   cached push: the list of the last push written into one client's cache,
+    #   then the whole cache applied (Sec. 2.3's re-apply of dropped values)
+    extra = torch.zeros_like(pool[0])
+    cached_ms = timed(lambda: fa.bfasgd_apply_cached(st, idx, val, cnt, extra, clients[st.T], ts[st.T]))
+    m_last = int(cnt.item())
+    #   fetch: selection over the server's theta, copied into a client's copy
+    def fetch():
+        fa.bfasgd_select_compact(st, theta, c, EPS_C, SEED ^ 0xFE7C, st.T, clients[st.T], idx, val, cnt, ws)
+        fa.bfasgd_apply_fetch(extra, idx, val, cnt)
+    fetch_ms = timed(fetch)
+    m_fetch = int(cnt.item())
+    #   synchronous SGD step with lambda = K clients (the Sec. 3 listing)
+    sync_st = fa.fasgd_init_state(theta, None, None, None, last_T, lam=K, alpha=w.alpha_sasgd)
+    sync_ms = timed(lambda: fa.sgd_sync_apply(sync_st, pool[:K], w.alpha_sasgd))
+    del extra
+
     # plain copy of one gradient buffer (4P bytes read, 4P written): the
     # bandwidth anchor, and the known-size kernel that calibrates the
     # rocprofv3 FETCH_SIZE / WRITE_SIZE counters
@@ -246,6 +274,12 @@ def main():
                                       "transmitted_fraction": m_avg / P},
             "bfasgd_apply_sparse": {"ms": sp_ms, "GB/s_algorithmic": sp_bytes / (sp_ms * 1e-3) / 1e9},
             "sasgd_apply_updates": {"ms": sas_ms_avg, "GB/s": sas_bytes / (sas_ms_avg * 1e-3) / 1e9},
+            "sgd_sync_apply": {"ms": sync_ms, "lambda": K,
+                               "GB/s": P * (8 + 4 * K) / (sync_ms * 1e-3) / 1e9},
+            "bfasgd_apply_cached": {"ms": cached_ms, "transmitted": m_last,
+                                    "GB/s_algorithmic": (36 * P + 12 * m_last) / (cached_ms * 1e-3) / 1e9},
+            "fetch_select_and_copy": {"ms": fetch_ms, "transmitted": m_fetch,
+                                      "GB/s_algorithmic": (8 * P + 20 * m_fetch) / (fetch_ms * 1e-3) / 1e9},
             "copy_anchor": {"GB/s": copy_gbs, "bytes": 8 * P},
         },
     }

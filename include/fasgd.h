@@ -185,6 +185,46 @@ fasgd_status bfasgd_apply_sparse(fasgd_state* st, const int32_t* idx, const floa
                                  const int64_t* d_count, int64_t capacity, int32_t client,
                                  int64_t grad_ts, hipStream_t stream);
 
+/*
+ * Synchronous SGD server (Sec. 3, the apply-update listing): with the
+ * gradients of all lambda clients collected, apply each one, in client
+ * order 0 .. lambda-1, as theta <- theta - lr * (g / lambda) (the division
+ * and the step are separate fp32 operations); then dense_T = T and T
+ * advances by one, since the weights changed once.  Reads and writes theta
+ * only (n, b, v may be NULL).
+ *   grads  host array of lambda device pointers, each fp32 [P]
+ *   lr     finite, > 0
+ */
+fasgd_status sgd_sync_apply(fasgd_state* st, const float* const* grads, float lr, hipStream_t stream);
+
+/*
+ * B-FASGD push with its dropped values re-applied: the server re-applies
+ * the client's most recent gradient (Sec. 2.3), kept per parameter.
+ * cache is this client's gradient cache, fp32 [P] (device, owned by the
+ * caller, zero before the client's first push).  The first
+ * min(*d_count, capacity) listed pairs are written into it
+ * (cache[idx[i]] = val[i]); then the whole cache is applied as one FASGD
+ * gradient at timestamp T with staleness T - grad_ts.  dense_T = T, T += 1.
+ * Indices outside [0, P) are skipped.  Errors: as bfasgd_apply_sparse, and
+ * FASGD_ERR_NULL for a NULL cache.
+ */
+fasgd_status bfasgd_apply_cached(fasgd_state* st, const int32_t* idx, const float* val,
+                                 const int64_t* d_count, int64_t capacity, float* cache,
+                                 int32_t client, int64_t grad_ts, hipStream_t stream);
+
+/*
+ * Fetch side of B-FASGD (Sec. 2.3): a client refreshes its copy of theta
+ * only where the transmit rule, with the fetch threshold, says so.  Select
+ * with bfasgd_select_compact, passing the server's theta as the values (and
+ * a seed that keeps fetch draws apart from push draws); this call then
+ * copies the listed values into the client's copy:
+ * theta_client[idx[i]] = val[i] for i < min(*d_count, capacity).  Indices
+ * outside [0, P) are skipped.  No state is changed.
+ *   theta_client  device fp32 [P]
+ */
+fasgd_status bfasgd_apply_fetch(float* theta_client, int64_t P, const int32_t* idx, const float* val,
+                                const int64_t* d_count, int64_t capacity, hipStream_t stream);
+
 /* Static text naming a status code. */
 const char* fasgd_status_string(fasgd_status s);
 

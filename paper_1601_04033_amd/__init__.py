@@ -6,7 +6,8 @@ libfasgd.so; torch provides device memory and the stream.  The functions
 keep the C ABI's names (include/fasgd.h):
 
     fasgd_init_state, fasgd_apply_updates, sasgd_apply_updates,
-    bfasgd_workspace_bytes, bfasgd_select_compact, bfasgd_apply_sparse
+    bfasgd_workspace_bytes, bfasgd_select_compact, bfasgd_apply_sparse,
+    sgd_sync_apply, bfasgd_apply_cached, bfasgd_apply_fetch
 
 There is no fallback: if libfasgd.so is missing or cannot be loaded, every
 call raises.
@@ -30,6 +31,7 @@ STATUS = {0: "FASGD_OK", 1: "FASGD_ERR_NULL", 2: "FASGD_ERR_ARG", 3: "FASGD_ERR_
 # every function include/fasgd.h declares
 ABI_FUNCTIONS = ("fasgd_init_state", "fasgd_apply_updates", "sasgd_apply_updates",
                  "bfasgd_workspace_bytes", "bfasgd_select_compact", "bfasgd_apply_sparse",
+                 "sgd_sync_apply", "bfasgd_apply_cached", "bfasgd_apply_fetch",
                  "fasgd_status_string", "fasgd_last_error")
 
 
@@ -70,8 +72,12 @@ def load_library(path: Optional[str] = None):
     lib.bfasgd_workspace_bytes.restype = sz
     lib.bfasgd_select_compact.argtypes = [S, P, f, f, u64, i64, i32, P, P, i64, P, P, sz, P]
     lib.bfasgd_apply_sparse.argtypes = [S, P, P, P, i64, i32, i64, P]
+    lib.sgd_sync_apply.argtypes = [S, P, f, P]
+    lib.bfasgd_apply_cached.argtypes = [S, P, P, P, i64, P, i32, i64, P]
+    lib.bfasgd_apply_fetch.argtypes = [P, i64, P, P, P, i64, P]
     for name in ("fasgd_init_state", "fasgd_apply_updates", "sasgd_apply_updates",
-                 "bfasgd_select_compact", "bfasgd_apply_sparse"):
+                 "bfasgd_select_compact", "bfasgd_apply_sparse", "sgd_sync_apply",
+                 "bfasgd_apply_cached", "bfasgd_apply_fetch"):
         getattr(lib, name).restype = ctypes.c_int
     lib.fasgd_status_string.argtypes = [ctypes.c_int]
     lib.fasgd_status_string.restype = ctypes.c_char_p
@@ -223,6 +229,47 @@ def bfasgd_apply_sparse(state: State, idx, val, d_count, client: int, grad_ts: i
     rc = load_library().bfasgd_apply_sparse(
         ctypes.byref(state.c), _dev_ptr(idx, torch.int32, "idx"), _dev_ptr(val, torch.float32, "val"),
         _dev_ptr(d_count, torch.int64, "d_count"), cap, int(client), int(grad_ts), _stream(stream))
+    _check(rc)
+
+
+def sgd_sync_apply(state: State, grads: Sequence, lr: float, stream=None) -> None:
+    """Synchronous SGD step with the gradients of all lambda clients; T advances by one."""
+    import torch
+    if len(grads) != int(state.c.lambda_):
+        raise ValueError(f"{len(grads)} gradients for lambda = {state.c.lambda_} clients")
+    ptrs = (ctypes.c_void_p * len(grads))()
+    for k, g in enumerate(grads):
+        if g.numel() != state.P:
+            raise ValueError(f"grads[{k}] has {g.numel()} elements, P = {state.P}")
+        ptrs[k] = _dev_ptr(g, torch.float32, f"grads[{k}]")
+    _check(load_library().sgd_sync_apply(ctypes.byref(state.c), ptrs, lr, _stream(stream)))
+
+
+def bfasgd_apply_cached(state: State, idx, val, d_count, cache, client: int, grad_ts: int, stream=None) -> None:
+    """Push with dropped values re-applied from the client's cache (updated in place)."""
+    import torch
+    cap = idx.numel()
+    if val.numel() != cap:
+        raise ValueError("idx and val must have the same capacity")
+    if cache.numel() != state.P:
+        raise ValueError("cache length differs from P")
+    rc = load_library().bfasgd_apply_cached(
+        ctypes.byref(state.c), _dev_ptr(idx, torch.int32, "idx"), _dev_ptr(val, torch.float32, "val"),
+        _dev_ptr(d_count, torch.int64, "d_count"), cap, _dev_ptr(cache, torch.float32, "cache"),
+        int(client), int(grad_ts), _stream(stream))
+    _check(rc)
+
+
+def bfasgd_apply_fetch(theta_client, idx, val, d_count, stream=None) -> None:
+    """Copy the listed values into a client's copy of theta."""
+    import torch
+    cap = idx.numel()
+    if val.numel() != cap:
+        raise ValueError("idx and val must have the same capacity")
+    rc = load_library().bfasgd_apply_fetch(
+        _dev_ptr(theta_client, torch.float32, "theta_client"), theta_client.numel(),
+        _dev_ptr(idx, torch.int32, "idx"), _dev_ptr(val, torch.float32, "val"),
+        _dev_ptr(d_count, torch.int64, "d_count"), cap, _stream(stream))
     _check(rc)
 
 

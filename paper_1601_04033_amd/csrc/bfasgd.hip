@@ -208,13 +208,8 @@ __global__ __launch_bounds__(kBlock) void select_scatter(const SelectArgs a)
     }
 }
 
-#ifndef SPARSE_E
-#define SPARSE_E 2
-#endif
-#ifndef SPARSE_CAP
-#define SPARSE_CAP 65536
-#endif
-constexpr int kSparseE = SPARSE_E;            // list entries per thread
+constexpr int kSparseE = 2;                   // list entries per lane
+constexpr int64_t kListMaxBlocks = 65536;     // grid cap of the list kernels (grid-stride)
 
 // A wave owns 64 E consecutive list entries and lane l takes entries
 // l, l + 64, ...: every gather instruction covers 64 consecutive entries
@@ -253,6 +248,20 @@ __global__ __launch_bounds__(kBlock) void sparse_apply(const SparseArgs a)
                 a.last_T[j[e]] = a.last_T_value;
             }
         }
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void scatter_list(float* __restrict__ dst, int64_t P,
+                                                       const int32_t* __restrict__ idx,
+                                                       const float* __restrict__ val,
+                                                       const int64_t* __restrict__ d_count, int64_t capacity)
+{
+    int64_t m = *d_count;
+    if (m > capacity) m = capacity;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < m; i += stride) {
+        const int64_t j = idx[i];
+        if (j >= 0 && j < P) dst[j] = val[i];
     }
 }
 
@@ -307,14 +316,25 @@ hipError_t launch_select(const SelectArgs& a, bool aligned, hipStream_t s)
 
 hipError_t launch_sparse(const SparseArgs& a, int mode, hipStream_t s)
 {
-    // enough threads for `capacity` entries; threads past the device count exit
+    // enough lanes for `capacity` entries (the count is only known on the
+    // device); lanes past the count exit
     int64_t g = (a.capacity + int64_t(kBlock) * kSparseE - 1) / (int64_t(kBlock) * kSparseE);
-    if (SPARSE_CAP > 0 && g > SPARSE_CAP) g = SPARSE_CAP;
+    if (g > kListMaxBlocks) g = kListMaxBlocks;
     if (g < 1) g = 1;
     if (mode == MATH_FAST)
         sparse_apply<MATH_FAST><<<static_cast<unsigned>(g), kBlock, 0, s>>>(a);
     else
         sparse_apply<MATH_IEEE><<<static_cast<unsigned>(g), kBlock, 0, s>>>(a);
+    return hipGetLastError();
+}
+
+hipError_t launch_scatter(float* dst, int64_t P, const int32_t* idx, const float* val,
+                          const int64_t* d_count, int64_t capacity, hipStream_t s)
+{
+    int64_t g = (capacity + kBlock - 1) / kBlock;
+    if (g > kListMaxBlocks) g = kListMaxBlocks;
+    if (g < 1) g = 1;
+    scatter_list<<<static_cast<unsigned>(g), kBlock, 0, s>>>(dst, P, idx, val, d_count, capacity);
     return hipGetLastError();
 }
 

@@ -156,6 +156,54 @@ __global__ __launch_bounds__(kBlock) void sasgd_dense_scalar(const DenseArgs a)
     a.theta[j] = th;
 }
 
+// Synchronous SGD (the apply-update listing of Sec. 3): every gradient is
+// divided by lambda, then theta <- theta - lr * that, in client order.
+__global__ __launch_bounds__(kBlock) void sync_sgd_vec(const DenseArgs a)
+{
+    const int K = a.K;
+    const float lam = a.lambda;
+    const int64_t nvec = a.P >> 2;
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    if (i < nvec) {
+        const int64_t o = i * 4;
+        f4 th = ld4(a.theta + o);
+        int k = 0;
+        for (; k + kBatch <= K; k += kBatch) {
+            f4 g[kBatch];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) g[u] = ld4(a.grad[k + u] + o);
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const float r = -a.coef[k + u];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) th[c] = fmaf(r, g[u][c] / lam, th[c]);
+            }
+        }
+        for (; k < K; ++k) {
+            const f4 g = ld4(a.grad[k] + o);
+            const float r = -a.coef[k];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) th[c] = fmaf(r, g[c] / lam, th[c]);
+        }
+        st4(a.theta + o, th);
+    } else if (i == nvec) {
+        for (int64_t j = nvec * 4; j < a.P; ++j) {
+            float th = a.theta[j];
+            for (int k = 0; k < K; ++k) th = fmaf(-a.coef[k], a.grad[k][j] / lam, th);
+            a.theta[j] = th;
+        }
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void sync_sgd_scalar(const DenseArgs a)
+{
+    const int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    if (j >= a.P) return;
+    float th = a.theta[j];
+    for (int k = 0; k < a.K; ++k) th = fmaf(-a.coef[k], a.grad[k][j] / a.lambda, th);
+    a.theta[j] = th;
+}
+
 }  // namespace
 
 hipError_t launch_init(float* n, float* b, float* v, int32_t* last_T, int64_t P,
@@ -189,6 +237,15 @@ hipError_t launch_sasgd_dense(const DenseArgs& a, bool aligned, hipStream_t s)
         sasgd_dense_vec<<<grid_for((a.P >> 2) + 1), kBlock, 0, s>>>(a);
     else
         sasgd_dense_scalar<<<grid_for(a.P), kBlock, 0, s>>>(a);
+    return hipGetLastError();
+}
+
+hipError_t launch_sync_sgd(const DenseArgs& a, bool aligned, hipStream_t s)
+{
+    if (aligned)
+        sync_sgd_vec<<<grid_for((a.P >> 2) + 1), kBlock, 0, s>>>(a);
+    else
+        sync_sgd_scalar<<<grid_for(a.P), kBlock, 0, s>>>(a);
     return hipGetLastError();
 }
 

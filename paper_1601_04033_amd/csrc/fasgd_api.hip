@@ -276,6 +276,95 @@ fasgd_status bfasgd_apply_sparse(fasgd_state* st, const int32_t* idx, const floa
     return ok();
 }
 
+fasgd_status sgd_sync_apply(fasgd_state* st, const float* const* grads, float lr, hipStream_t stream)
+{
+    fasgd_status s = check_state(st, false);
+    if (s != FASGD_OK) return s;
+    if (!grads) return fail(FASGD_ERR_NULL, "grads is NULL");
+    if (!(isfinite(lr) && lr > 0.0f)) return fail(FASGD_ERR_ARG, "lr must be finite and > 0");
+    if (st->T + 1 > INT32_MAX) return fail(FASGD_ERR_ARG, "T exceeds the int32 timestamp range");
+    bool vec = aligned(st->theta, 16);
+    for (int32_t k = 0; k < st->lambda; ++k) {
+        if (!grads[k]) return fail(FASGD_ERR_NULL, "grads[%d] is NULL", k);
+        if (!aligned(grads[k], 4)) return fail(FASGD_ERR_ALIGN, "grads[%d] is not 4-byte aligned", k);
+        vec = vec && aligned(grads[k], 16);
+    }
+    // lambda gradients in passes of at most FASGD_MAX_K; theta is stored in
+    // fp32 between passes exactly as it is held in registers within one
+    for (int32_t k0 = 0; k0 < st->lambda; k0 += FASGD_MAX_K) {
+        fasgd::DenseArgs a;
+        memset(&a, 0, sizeof a);
+        const int32_t K = st->lambda - k0 < FASGD_MAX_K ? st->lambda - k0 : FASGD_MAX_K;
+        for (int32_t k = 0; k < K; ++k) {
+            a.grad[k] = grads[k0 + k];
+            a.coef[k] = lr;
+        }
+        a.theta = st->theta;
+        a.P = st->P;
+        a.K = K;
+        a.lambda = static_cast<float>(st->lambda);
+        const hipError_t e = fasgd::launch_sync_sgd(a, vec, stream);
+        if (e != hipSuccess) return hip_fail(e, "sgd_sync_apply");
+    }
+    st->dense_T = st->T;
+    st->T += 1;
+    return ok();
+}
+
+fasgd_status bfasgd_apply_cached(fasgd_state* st, const int32_t* idx, const float* val, const int64_t* d_count,
+                                 int64_t capacity, float* cache, int32_t client, int64_t grad_ts,
+                                 hipStream_t stream)
+{
+    fasgd_status s = check_state(st, true);
+    if (s != FASGD_OK) return s;
+    if (!d_count || !cache) return fail(FASGD_ERR_NULL, "d_count or cache is NULL");
+    if (capacity < 0) return fail(FASGD_ERR_ARG, "capacity must be >= 0");
+    if (capacity > 0 && (!idx || !val)) return fail(FASGD_ERR_NULL, "idx or val is NULL");
+    if ((idx && !aligned(idx, 4)) || (val && !aligned(val, 4)) || !aligned(d_count, 8) || !aligned(cache, 4))
+        return fail(FASGD_ERR_ALIGN, "misaligned idx, val, d_count or cache");
+    float tau_div;
+    s = staleness(st, &client, &grad_ts, 1, &tau_div);
+    if (s != FASGD_OK) return s;
+    if (capacity > 0) {
+        const hipError_t e = fasgd::launch_scatter(cache, st->P, idx, val, d_count, capacity, stream);
+        if (e != hipSuccess) return hip_fail(e, "bfasgd_apply_cached (cache update)");
+    }
+    fasgd::DenseArgs a;
+    memset(&a, 0, sizeof a);
+    a.theta = st->theta;
+    a.n = st->n;
+    a.b = st->b;
+    a.v = st->v;
+    a.grad[0] = cache;
+    a.coef[0] = st->math_mode == FASGD_MATH_FAST ? st->alpha / tau_div : tau_div;
+    a.P = st->P;
+    a.K = 1;
+    a.h = hyper_of(st);
+    const bool vec = aligned(st->theta, 16) && aligned(st->n, 16) && aligned(st->b, 16) && aligned(st->v, 16) &&
+                     aligned(cache, 16);
+    const hipError_t e = fasgd::launch_fasgd_dense(a, st->math_mode, vec, stream);
+    if (e != hipSuccess) return hip_fail(e, "bfasgd_apply_cached");
+    st->dense_T = st->T;
+    st->T += 1;
+    return ok();
+}
+
+fasgd_status bfasgd_apply_fetch(float* theta_client, int64_t P, const int32_t* idx, const float* val,
+                                const int64_t* d_count, int64_t capacity, hipStream_t stream)
+{
+    if (!theta_client || !d_count) return fail(FASGD_ERR_NULL, "theta_client or d_count is NULL");
+    if (P < 1) return fail(FASGD_ERR_ARG, "P = %lld must be >= 1", (long long)P);
+    if (capacity < 0) return fail(FASGD_ERR_ARG, "capacity must be >= 0");
+    if (capacity > 0 && (!idx || !val)) return fail(FASGD_ERR_NULL, "idx or val is NULL");
+    if (!aligned(theta_client, 4) || (idx && !aligned(idx, 4)) || (val && !aligned(val, 4)) || !aligned(d_count, 8))
+        return fail(FASGD_ERR_ALIGN, "misaligned theta_client, idx, val or d_count");
+    if (capacity > 0) {
+        const hipError_t e = fasgd::launch_scatter(theta_client, P, idx, val, d_count, capacity, stream);
+        if (e != hipSuccess) return hip_fail(e, "bfasgd_apply_fetch");
+    }
+    return ok();
+}
+
 const char* fasgd_status_string(fasgd_status s)
 {
     switch (s) {

@@ -22,6 +22,7 @@ struct DenseArgs {
     float coef[kMaxK];      // FASGD IEEE: tau_k; FASGD FAST and SASGD: alpha / tau_k
     int64_t P;
     int32_t K;
+    float lambda;           // synchronous SGD: gradients are divided by lambda
     Hyper h;
 };
 
@@ -29,6 +30,8 @@ hipError_t launch_init(float* n, float* b, float* v, int32_t* last_T, int64_t P,
                        float n0, float b0, float v0, hipStream_t s);
 hipError_t launch_fasgd_dense(const DenseArgs& a, int mode, bool aligned, hipStream_t s);
 hipError_t launch_sasgd_dense(const DenseArgs& a, bool aligned, hipStream_t s);
+// theta <- theta - coef[k] * (g_k / lambda), k in order (coef[k] = lr)
+hipError_t launch_sync_sgd(const DenseArgs& a, bool aligned, hipStream_t s);
 
 // B-FASGD selection: Philox decisions -> per-wave ballots and per-tile
 // counts, an exclusive scan of the tile counts, then ordered writes.
@@ -75,5 +78,10 @@ struct SparseArgs {
 };
 
 hipError_t launch_sparse(const SparseArgs& a, int mode, hipStream_t s);
+
+// dst[idx[i]] = val[i] for i < min(*d_count, capacity); indices outside
+// [0, P) are skipped.
+hipError_t launch_scatter(float* dst, int64_t P, const int32_t* idx, const float* val,
+                          const int64_t* d_count, int64_t capacity, hipStream_t s);
 
 }  // namespace fasgd

@@ -194,3 +194,36 @@ def test_sparse_rejects_bad_arguments(lib):
     assert sp(count=None) == 1
     assert sp(count=cntp + 4) == 5
     assert st.T == 2
+
+
+def test_next_entry_points_reject_bad_arguments(lib):
+    st, f = _state(P=16, lam=3, T=2)
+    g = (ctypes.c_void_p * 3)(f.ptr(5), f.ptr(5), f.ptr(5))
+    assert lib.sgd_sync_apply(ctypes.byref(st), None, 0.1, None) == 1
+    assert lib.sgd_sync_apply(ctypes.byref(st), g, 0.0, None) == 2
+    assert lib.sgd_sync_apply(ctypes.byref(st), g, float("inf"), None) == 2
+    gnull = (ctypes.c_void_p * 3)(f.ptr(5), None, f.ptr(5))
+    assert lib.sgd_sync_apply(ctypes.byref(st), gnull, 0.1, None) == 1
+    gmis = (ctypes.c_void_p * 3)(f.ptr(5), f.ptr(5, misalign=2), f.ptr(5))
+    assert lib.sgd_sync_apply(ctypes.byref(st), gmis, 0.1, None) == 5
+    cnt = np.zeros(2, np.int64)
+    cntp = (cnt.ctypes.data + 7) & ~7
+
+    def cached(cache=f.ptr(5), client=0, ts=0, cap=16):
+        return lib.bfasgd_apply_cached(ctypes.byref(st), f.ptr(0), f.ptr(1), cntp, cap, cache, client, ts, None)
+
+    assert cached(cache=None) == 1
+    assert cached(ts=3) == 3
+    assert cached(client=3) == 4
+    assert cached(cap=-1) == 2
+    assert cached(cache=f.ptr(5, misalign=1)) == 5
+
+    def fetch(dst=f.ptr(2), P=16, cap=16, count=cntp):
+        return lib.bfasgd_apply_fetch(dst, P, f.ptr(0), f.ptr(1), count, cap, None)
+
+    assert fetch(dst=None) == 1
+    assert fetch(P=0) == 2
+    assert fetch(cap=-3) == 2
+    assert fetch(count=None) == 1
+    assert fetch(dst=f.ptr(2, misalign=2)) == 5
+    assert st.T == 2

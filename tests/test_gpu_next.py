@@ -1,0 +1,114 @@
+"""GPU parity of the widened server paths: the synchronous-SGD server
+(Sec. 3 listing), pushes with dropped values re-applied from the client's
+cache (Sec. 2.3), and fetch-side selection of theta (Sec. 2.3)."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1601_04033_amd as fa
+import workload
+from helpers import RTOL_ONE, RTOL_SEQ, assert_close, assert_state_close, gpu, new_gpu_state, sample_indices, to_dev
+
+pytestmark = pytest.mark.gpu
+SEED = 0xF00D
+
+
+@pytest.mark.parametrize("lam,P", [(16, workload.MLP_P), (1, 10_001), (100, 40_003)])
+def test_sync_sgd_matches_oracle(lam, P):
+    """Three synchronous steps; lambda = 100 exercises passes of 64 gradients."""
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["mlp"]
+    theta0, m, s = workload.host_params(w, P)
+    st = new_gpu_state(theta0, dev, lam, 0.04, fa.MATH_FAST, sasgd=True)
+    ref = oracle.init_state(theta0, alpha=0.04)
+    lr = 0.04
+    for step in range(3):
+        grads = [workload.host_gradient(w, m, s, step * lam + k) for k in range(lam)]
+        fa.sgd_sync_apply(st, [to_dev(g, dev) for g in grads], lr)
+        oracle.sync_sgd_apply(ref, grads, lr)
+        if step == 0:
+            torch.cuda.synchronize()
+            assert_close(st.theta.cpu().numpy(), ref.theta, RTOL_ONE, what="after one step")
+    torch.cuda.synchronize()
+    assert_close(st.theta.cpu().numpy(), ref.theta, RTOL_SEQ, what="after three steps")
+    assert st.T == ref.T == 3 and st.dense_T == 2
+    np.testing.assert_array_equal(st.last_update().cpu().numpy(), ref.last_T)
+
+
+def test_sync_sgd_rejects_a_missing_gradient_list():
+    dev = gpu()
+    st = new_gpu_state(np.zeros(100, np.float32), dev, 4, 0.01, fa.MATH_FAST, sasgd=True)
+    import torch
+    with pytest.raises(ValueError):
+        fa.sgd_sync_apply(st, [torch.zeros(100, device=dev)] * 3, 0.1)
+
+
+@pytest.mark.parametrize("mode", [fa.MATH_FAST, fa.MATH_IEEE])
+def test_cached_pushes_match_oracle(mode):
+    """MLP layout, lambda = 16, 40 pushes at about 20 %: every push writes its
+    list into the client's cache and applies the whole cache.  Both sides get
+    the same lists (the oracle's selection on its own v), so the comparison
+    isolates the cached apply; the selection itself is tested elsewhere."""
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["mlp_bfasgd"]
+    P, U = 300_007, 40
+    theta0, m_, s_ = workload.host_params(w, P)
+    clients, ts = workload.schedule(w, U)
+    st = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, mode)
+    ref = oracle.init_state(theta0, alpha=w.alpha_fasgd)
+    caches_gpu = torch.zeros(w.lam, P, device=dev)
+    caches_ref = np.zeros((w.lam, P), np.float32)
+    cnt = torch.zeros(1, device=dev, dtype=torch.int64)
+    for t in range(U):
+        g = workload.host_gradient(w, m_, s_, t)
+        c = 0.0 if t < w.lam else 4.0 * float(np.median(ref.v))          # every client's first push is complete
+        idx, val, mm = oracle.bfasgd_select(ref.v.astype(np.float32), g, c, 1e-8, SEED, ref.T, clients[t])
+        cl = int(clients[t])
+        cache_row = caches_ref[cl].copy()
+        oracle.bfasgd_apply_cached(ref, cache_row, idx, val, ts[t])
+        caches_ref[cl] = cache_row
+        cnt.fill_(mm)
+        fa.bfasgd_apply_cached(st, to_dev(idx, dev) if mm else torch.zeros(1, device=dev, dtype=torch.int32),
+                               to_dev(val, dev) if mm else torch.zeros(1, device=dev), cnt, caches_gpu[cl], cl, ts[t])
+        if t == 0:
+            torch.cuda.synchronize()
+            assert_state_close(st, ref, RTOL_ONE, what="after one push")
+    torch.cuda.synchronize()
+    assert_state_close(st, ref, RTOL_SEQ, what=f"after {U} pushes")
+    np.testing.assert_array_equal(caches_gpu.cpu().numpy(), caches_ref)
+    assert st.dense_T == U - 1
+
+
+def test_fetch_selection_refreshes_client_copy_bit_exact():
+    """A client's copy of theta refreshed where the fetch rule says so: the
+    server's theta is the value array of the selection."""
+    import torch
+    dev = gpu()
+    P = 1_000_003
+    rng = np.random.default_rng(12)
+    theta_srv = rng.standard_normal(P).astype(np.float32)
+    v = workload.synthetic_v(P, seed=12)
+    client = (theta_srv + rng.standard_normal(P).astype(np.float32)).astype(np.float32)
+    st = new_gpu_state(theta_srv, dev, 8, 0.005, fa.MATH_FAST)
+    st.v.copy_(torch.from_numpy(v))
+    copy_gpu = to_dev(client, dev)
+    idx = torch.empty(P, device=dev, dtype=torch.int32)
+    val = torch.empty(P, device=dev)
+    cnt = torch.zeros(1, device=dev, dtype=torch.int64)
+    ws = fa.allocate_workspace(P, dev)
+    fetch_seed = SEED ^ 0xFE7C000000000000
+    fa.bfasgd_select_compact(st, st.theta, 30.0, 1e-8, fetch_seed, 5, 3, idx, val, cnt, ws)
+    fa.bfasgd_apply_fetch(copy_gpu, idx, val, cnt)
+    torch.cuda.synchronize()
+    r_idx, r_val, r_m = oracle.bfasgd_select(v, theta_srv, 30.0, 1e-8, fetch_seed, 5, 3)
+    expect = client.copy()
+    expect[r_idx] = r_val
+    assert int(cnt.item()) == r_m and 0 < r_m < P
+    np.testing.assert_array_equal(copy_gpu.cpu().numpy().view(np.uint32), expect.view(np.uint32))
+    # c = 0: the copy becomes the server's theta exactly
+    fa.bfasgd_select_compact(st, st.theta, 0.0, 1e-8, fetch_seed, 6, 3, idx, val, cnt, ws)
+    fa.bfasgd_apply_fetch(copy_gpu, idx, val, cnt)
+    torch.cuda.synchronize()
+    assert torch.equal(copy_gpu, st.theta)
