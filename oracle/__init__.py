@@ -49,6 +49,10 @@ def _load():
     lib.oracle_sync_sgd_apply.restype = None
     lib.oracle_bfasgd_apply_cached.argtypes = [i64, dp, dp, dp, dp, i64p, i64p, fp, i32p, fp, i64, i64, d, d, d, d]
     lib.oracle_bfasgd_apply_cached.restype = ctypes.c_int
+    lib.oracle_bfasgd_decide_segments.argtypes = [i64, i64p, fp, f, f, u64, i64, i32, u8p, dp]
+    lib.oracle_bfasgd_decide_segments.restype = None
+    lib.oracle_bfasgd_apply_segments.argtypes = [i64, i64p, u8p, dp, dp, dp, dp, i64p, i64p, fp, i64, d, d, d, d]
+    lib.oracle_bfasgd_apply_segments.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -242,6 +246,50 @@ def bfasgd_apply_cached(st: State, cache, idx, val, grad_ts: int) -> None:
                                         _ptr(cache, ctypes.c_float), _ptr(idx, ctypes.c_int32),
                                         _ptr(val, ctypes.c_float), idx.shape[0], int(grad_ts),
                                         h["alpha"], h["gamma"], h["beta"], h["eps"])
+    if rc != 0:
+        raise OracleError(f"negative staleness: grad_ts={grad_ts} > T={st.T}")
+    st.T = T.value
+
+
+def _segments(seg, P):
+    seg = np.ascontiguousarray(seg, dtype=np.int64)
+    if seg.ndim != 1 or seg.size < 2 or seg[0] != 0 or seg[-1] != P or (np.diff(seg) <= 0).any():
+        raise OracleError("segments must be 0 = seg[0] < seg[1] < ... < seg[S] = P")
+    return seg
+
+
+def bfasgd_decide_segments(v, seg, c, eps_c, seed, T, client):
+    """Paper-literal decisions (Sec. 2.3 / Sec. 5): one per segment from the
+    segment's mean of v (fp32 values, summed in fp64).  Returns (bool [S],
+    mean fp64 [S])."""
+    lib = _load()
+    v = np.ascontiguousarray(v, dtype=np.float32)
+    seg = _segments(seg, v.shape[0])
+    S = seg.size - 1
+    out = np.zeros(S, np.uint8)
+    mean = np.zeros(S, np.float64)
+    lib.oracle_bfasgd_decide_segments(S, _ptr(seg, ctypes.c_int64), _ptr(v, ctypes.c_float), f32(c), f32(eps_c),
+                                      int(seed) & (2**64 - 1), int(T), int(client), _ptr(out, ctypes.c_uint8),
+                                      _ptr(mean, ctypes.c_double))
+    return out.astype(bool), mean
+
+
+def bfasgd_apply_segments(st: State, grad, seg, transmit, grad_ts: int) -> None:
+    """FASGD update on the transmitted segments only; T advances by one."""
+    lib = _load()
+    grad = np.ascontiguousarray(grad, dtype=np.float32)
+    seg = _segments(seg, st.P)
+    tr = np.ascontiguousarray(transmit, dtype=np.uint8)
+    if tr.size != seg.size - 1 or grad.shape != (st.P,):
+        raise OracleError("shape mismatch")
+    T = ctypes.c_int64(st.T)
+    h = st.hyper
+    rc = lib.oracle_bfasgd_apply_segments(seg.size - 1, _ptr(seg, ctypes.c_int64), _ptr(tr, ctypes.c_uint8),
+                                          _ptr(st.theta, ctypes.c_double), _ptr(st.n, ctypes.c_double),
+                                          _ptr(st.b, ctypes.c_double), _ptr(st.v, ctypes.c_double),
+                                          _ptr(st.last_T, ctypes.c_int64), ctypes.byref(T),
+                                          _ptr(grad, ctypes.c_float), int(grad_ts),
+                                          h["alpha"], h["gamma"], h["beta"], h["eps"])
     if rc != 0:
         raise OracleError(f"negative staleness: grad_ts={grad_ts} > T={st.T}")
     st.T = T.value

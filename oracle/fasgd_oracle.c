@@ -251,3 +251,61 @@ int oracle_bfasgd_apply_cached(int64_t P, double *theta, double *n, double *b, d
         cache[idx[i]] = val[i];
     return oracle_fasgd_apply(P, theta, n, b, v, last_T, T, cache, grad_ts, alpha, gamma, beta, eps);
 }
+
+/* ------------------------------------------------------------------------- */
+/* B-FASGD as the paper states it (Sec. 2.3): one decision per push or fetch  */
+/* opportunity, from v averaged over all the parameters; per tensor (Sec. 5), */
+/* one decision per segment [seg[s], seg[s+1]) from that segment's mean.      */
+/* Decided in fp64: t = mean + eps, u = t + c, transmit iff r * u < t, with r */
+/* the top 24 bits of word 0 of Philox4x32-10 at counter                      */
+/* (s low, 0x80000000 | s high, T, client) (the set top bit keeps these draws */
+/* apart from the per-parameter ones, whose second word is j / 2^34 = 0).     */
+/* ------------------------------------------------------------------------- */
+void oracle_bfasgd_decide_segments(int64_t S, const int64_t *seg, const float *v, float c,
+                                   float eps_c, uint64_t seed, int64_t T, int32_t client,
+                                   uint8_t *transmit, double *mean_out)
+{
+    uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    for (int64_t s = 0; s < S; ++s) {
+        double sum = 0.0;
+        for (int64_t j = seg[s]; j < seg[s + 1]; ++j)
+            sum += (double)v[j];
+        double mean = sum / (double)(seg[s + 1] - seg[s]);
+        uint32_t ctr[4] = {(uint32_t)s, 0x80000000u | (uint32_t)((uint64_t)s >> 32), (uint32_t)T,
+                           (uint32_t)client};
+        uint32_t w[4];
+        oracle_philox4x32_10(ctr, key, w);
+        double r = (double)(w[0] >> 8) * 0x1p-24;
+        double t = mean + (double)eps_c;
+        double u = t + (double)c;
+        transmit[s] = (uint8_t)(fma(r, u, -t) < 0.0);
+        if (mean_out)
+            mean_out[s] = mean;
+    }
+}
+
+/*
+ * Server side of a push decided per segment: the FASGD update (Sec. 2.2) on
+ * the transmitted segments, nothing elsewhere; T advances by one.
+ */
+int oracle_bfasgd_apply_segments(int64_t S, const int64_t *seg, const uint8_t *transmit,
+                                 double *theta, double *n, double *b, double *v, int64_t *last_T,
+                                 int64_t *T, const float *grad, int64_t grad_ts, double alpha,
+                                 double gamma, double beta, double eps)
+{
+    double tau_div;
+    if (staleness_divisor(*T, grad_ts, &tau_div) != 0)
+        return -1;
+    for (int64_t s = 0; s < S; ++s) {
+        if (!transmit[s])
+            continue;
+        for (int64_t j = seg[s]; j < seg[s + 1]; ++j) {
+            fasgd_update_one(&theta[j], &n[j], &b[j], &v[j], (double)grad[j],
+                             alpha, gamma, beta, eps, tau_div);
+            if (last_T)
+                last_T[j] = *T;
+        }
+    }
+    *T += 1;
+    return 0;
+}

@@ -86,3 +86,83 @@ def test_dropped_push_reapplies_the_most_recent_gradient():
     for name in ("theta", "n", "b", "v", "last_T"):
         np.testing.assert_array_equal(getattr(a, name), getattr(b, name))
     assert b.T == 3
+
+
+# ------------------------------------------------ paper-literal mean-v decision
+from fractions import Fraction  # noqa: E402
+
+
+def _seg_r(s, seed, T, client):
+    w = oracle.philox4x32_10([s & 0xFFFFFFFF, 0x80000000 | (s >> 32), T & 0xFFFFFFFF, client],
+                             [seed & 0xFFFFFFFF, seed >> 32])[0]
+    return Fraction(int(w) >> 8, 1 << 24)
+
+
+def test_segment_decision_matches_exact_rule_with_exact_mean():
+    """r < 1/(1 + c/(mean + eps)) with the mean of the fp32 v values taken
+    exactly: the fp64 decision agrees outside a 2^-40 relative margin."""
+    rng = np.random.default_rng(21)
+    P = 3000
+    v = np.exp(rng.uniform(np.log(1e-3), np.log(1e3), P)).astype(np.float32)
+    seg = np.unique(np.concatenate([[0, P], rng.integers(1, P, 40)])).astype(np.int64)
+    near = 0
+    for T, client, c in [(0, 0, 1.0), (7, 3, 30.0), (123456, 11, 0.01), (2 ** 32 - 1, 5, 400.0)]:
+        dec, mean = oracle.bfasgd_decide_segments(v, seg, c, 1e-8, 0xABCDEF, T, client)
+        for s in range(seg.size - 1):
+            lo, hi = seg[s], seg[s + 1]
+            exact_mean = sum(Fraction(float(x)) for x in v[lo:hi]) / (hi - lo)
+            assert abs(Fraction(mean[s]) - exact_mean) <= exact_mean * Fraction(1, 2 ** 44)
+            t = exact_mean + Fraction(float(np.float32(1e-8)))
+            p = t / (t + Fraction(float(np.float32(c))))
+            r = _seg_r(s, 0xABCDEF, T, client)
+            if abs(r - p) <= p * Fraction(1, 2 ** 40):
+                near += 1
+                continue
+            assert dec[s] == (r < p), (T, s)
+    assert near == 0
+
+
+def test_segment_decision_constant_v_limits_and_independence():
+    P = 4096
+    seg = np.array([0, 1, 100, 4000, 4096], np.int64)
+    v = np.full(P, 2.5, np.float32)
+    dec, mean = oracle.bfasgd_decide_segments(v, seg, 1.0, 0.0, 9, 4, 1)
+    assert (mean == 2.5).all()
+    assert oracle.bfasgd_decide_segments(v, seg, 0.0, 1e-8, 9, 4, 1)[0].all()          # c = 0
+    assert oracle.bfasgd_decide_segments(np.full(P, 1e30, np.float32), seg, 5.0, 1e-8, 9, 4, 1)[0].all()
+    assert not oracle.bfasgd_decide_segments(np.zeros(P, np.float32), seg, 5.0, 1e-30, 9, 4, 1)[0].any()
+    # a segment's decision depends on its own v only
+    v2 = v.copy()
+    v2[100:4000] = 1e-6
+    d2, _ = oracle.bfasgd_decide_segments(v2, seg, 1.0, 0.0, 9, 4, 1)
+    assert d2[0] == dec[0] and d2[1] == dec[1] and d2[3] == dec[3]
+
+
+def test_segment_decision_rate():
+    """Over many opportunities (timestamps) the transmit frequency is
+    1/(1 + c/(mean + eps)) (binomial z-test)."""
+    P = 64
+    v = np.full(P, 3.0, np.float32)
+    seg = np.array([0, P], np.int64)
+    c = 7.0
+    hits = sum(bool(oracle.bfasgd_decide_segments(v, seg, c, 0.0, 77, T, 2)[0][0]) for T in range(20000))
+    p = 3.0 / (3.0 + c)
+    z = (hits - 20000 * p) / np.sqrt(20000 * p * (1 - p))
+    assert abs(z) < 5, (hits, z)
+
+
+def test_apply_segments_all_and_none():
+    theta0, grads = _problem(P=700, lam=3)
+    seg = np.array([0, 10, 300, 700], np.int64)
+    a = oracle.init_state(theta0, alpha=0.005)
+    b = oracle.init_state(theta0, alpha=0.005)
+    oracle.fasgd_apply(a, grads[0], 0)
+    oracle.bfasgd_apply_segments(b, grads[0], seg, np.ones(3, bool), 0)
+    for name in ("theta", "n", "b", "v", "last_T"):
+        np.testing.assert_array_equal(getattr(a, name), getattr(b, name))
+    before = b.copy()
+    oracle.bfasgd_apply_segments(b, grads[1], seg, np.array([False, True, False]), 1)
+    for name in ("theta", "n", "b", "v", "last_T"):
+        np.testing.assert_array_equal(getattr(b, name)[:10], getattr(before, name)[:10])
+        np.testing.assert_array_equal(getattr(b, name)[300:], getattr(before, name)[300:])
+    assert (b.last_T[10:300] == 1).all() and b.T == 2
