@@ -228,6 +228,16 @@ def main():
         fa.bfasgd_apply_fetch(extra, idx, val, cnt)
     fetch_ms = timed(fetch)
     m_fetch = int(cnt.item())
+    #   the paper's own decision: one per push from the mean of v, and one per
+    #   segment for 64 equal segments; then the push applied on the sent ones
+    seg1 = np.array([0, P], np.int64)
+    seg64 = np.linspace(0, P, 65).astype(np.int64)
+    dsel = torch.zeros(64, device=dev, dtype=torch.uint8)
+    wseg = torch.empty(fa.bfasgd_segments_workspace_bytes(P, 64), device=dev, dtype=torch.uint8)
+    dec1_ms = timed(lambda: fa.bfasgd_decide_segments(st, seg1, c, EPS_C, SEED, st.T, 0, dsel[:1], wseg))
+    dec64_ms = timed(lambda: fa.bfasgd_decide_segments(st, seg64, c, EPS_C, SEED, st.T, 0, dsel, wseg))
+    dsel.fill_(1)
+    segapply_ms = timed(lambda: fa.bfasgd_apply_segments(st, pool[K], seg64, dsel, clients[st.T], ts[st.T]))
     #   synchronous SGD step with lambda = K clients (the Sec. 3 listing)
     sync_st = fa.fasgd_init_state(theta, None, None, None, last_T, lam=K, alpha=w.alpha_sasgd)
     sync_ms = timed(lambda: fa.sgd_sync_apply(sync_st, pool[:K], w.alpha_sasgd))
@@ -280,6 +290,10 @@ def main():
                                     "GB/s_algorithmic": (36 * P + 12 * m_last) / (cached_ms * 1e-3) / 1e9},
             "fetch_select_and_copy": {"ms": fetch_ms, "transmitted": m_fetch,
                                       "GB/s_algorithmic": (8 * P + 20 * m_fetch) / (fetch_ms * 1e-3) / 1e9},
+            "bfasgd_decide_segments": {"ms_whole_vector": dec1_ms, "ms_64_segments": dec64_ms,
+                                       "GB/s": 4 * P / (dec1_ms * 1e-3) / 1e9},
+            "bfasgd_apply_segments": {"ms_all_sent": segapply_ms,
+                                      "GB/s": 40 * P / (segapply_ms * 1e-3) / 1e9},
             "copy_anchor": {"GB/s": copy_gbs, "bytes": 8 * P},
         },
     }

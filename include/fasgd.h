@@ -225,6 +225,40 @@ fasgd_status bfasgd_apply_cached(fasgd_state* st, const int32_t* idx, const floa
 fasgd_status bfasgd_apply_fetch(float* theta_client, int64_t P, const int32_t* idx, const float* val,
                                 const int64_t* d_count, int64_t capacity, hipStream_t stream);
 
+/*
+ * B-FASGD decision as the paper states it (Sec. 2.3): one decision per push
+ * (or fetch) opportunity, from v averaged over all parameters; or, per
+ * tensor (Sec. 5), one decision per segment s = [seg[s], seg[s+1]) from that
+ * segment's mean of v.  In fp64: mean_s = (sum of v over s) / its length,
+ * t = mean_s + eps_c, u = t + c, transmit <=> r_s * u - t < 0 (one rounding),
+ * where r_s is the top 24 bits of word 0 of Philox4x32-10 at counter
+ * (s low 32 bits, 0x80000000 | s high bits, T, client) with key (seed low,
+ * seed high), scaled by 2^-24 (the set top bit keeps these draws apart
+ * from the per-parameter ones).  d_transmit[s] receives 1 or 0.
+ *   seg        host int64 [S+1], 0 = seg[0] < seg[1] < ... < seg[S] = P
+ *   S          >= 1 (1 = the whole parameter vector)
+ *   d_transmit device uint8 [S]
+ *   workspace  device scratch of bfasgd_segments_workspace_bytes(P, S)
+ *              bytes, 256-byte aligned, contents irrelevant
+ * The sums are fp64 in a fixed order, so the result is the same run to run.
+ * Other arguments and errors as bfasgd_select_compact.
+ */
+size_t bfasgd_segments_workspace_bytes(int64_t P, int32_t S);
+fasgd_status bfasgd_decide_segments(const fasgd_state* st, const int64_t* seg, int32_t S, float c, float eps_c,
+                                    uint64_t seed, int64_t T, int32_t client, uint8_t* d_transmit,
+                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Server side of a push decided per segment: the FASGD update of
+ * fasgd_apply_updates, at timestamp T with staleness T - grad_ts, on the
+ * segments with d_transmit[s] = 1 (their parameters get last_T = T) and
+ * nothing on the others (Sec. 2.3 drops the push there); T advances by one.
+ *   grad  device fp32 [P];  seg, S as bfasgd_decide_segments
+ */
+fasgd_status bfasgd_apply_segments(fasgd_state* st, const float* grad, const int64_t* seg, int32_t S,
+                                   const uint8_t* d_transmit, int32_t client, int64_t grad_ts,
+                                   hipStream_t stream);
+
 /* Static text naming a status code. */
 const char* fasgd_status_string(fasgd_status s);
 

@@ -32,6 +32,7 @@ STATUS = {0: "FASGD_OK", 1: "FASGD_ERR_NULL", 2: "FASGD_ERR_ARG", 3: "FASGD_ERR_
 ABI_FUNCTIONS = ("fasgd_init_state", "fasgd_apply_updates", "sasgd_apply_updates",
                  "bfasgd_workspace_bytes", "bfasgd_select_compact", "bfasgd_apply_sparse",
                  "sgd_sync_apply", "bfasgd_apply_cached", "bfasgd_apply_fetch",
+                 "bfasgd_segments_workspace_bytes", "bfasgd_decide_segments", "bfasgd_apply_segments",
                  "fasgd_status_string", "fasgd_last_error")
 
 
@@ -75,9 +76,14 @@ def load_library(path: Optional[str] = None):
     lib.sgd_sync_apply.argtypes = [S, P, f, P]
     lib.bfasgd_apply_cached.argtypes = [S, P, P, P, i64, P, i32, i64, P]
     lib.bfasgd_apply_fetch.argtypes = [P, i64, P, P, P, i64, P]
+    lib.bfasgd_segments_workspace_bytes.argtypes = [i64, i32]
+    lib.bfasgd_segments_workspace_bytes.restype = sz
+    lib.bfasgd_decide_segments.argtypes = [S, P, i32, f, f, u64, i64, i32, P, P, sz, P]
+    lib.bfasgd_apply_segments.argtypes = [S, P, P, i32, P, i32, i64, P]
     for name in ("fasgd_init_state", "fasgd_apply_updates", "sasgd_apply_updates",
                  "bfasgd_select_compact", "bfasgd_apply_sparse", "sgd_sync_apply",
-                 "bfasgd_apply_cached", "bfasgd_apply_fetch"):
+                 "bfasgd_apply_cached", "bfasgd_apply_fetch", "bfasgd_decide_segments",
+                 "bfasgd_apply_segments"):
         getattr(lib, name).restype = ctypes.c_int
     lib.fasgd_status_string.argtypes = [ctypes.c_int]
     lib.fasgd_status_string.restype = ctypes.c_char_p
@@ -270,6 +276,43 @@ def bfasgd_apply_fetch(theta_client, idx, val, d_count, stream=None) -> None:
         _dev_ptr(theta_client, torch.float32, "theta_client"), theta_client.numel(),
         _dev_ptr(idx, torch.int32, "idx"), _dev_ptr(val, torch.float32, "val"),
         _dev_ptr(d_count, torch.int64, "d_count"), cap, _stream(stream))
+    _check(rc)
+
+
+def _seg_array(seg):
+    import numpy as np
+    a = np.ascontiguousarray(seg, dtype=np.int64)
+    return a, a.ctypes.data_as(ctypes.c_void_p), a.size - 1
+
+
+def bfasgd_segments_workspace_bytes(P: int, S: int) -> int:
+    return int(load_library().bfasgd_segments_workspace_bytes(int(P), int(S)))
+
+
+def bfasgd_decide_segments(state: State, seg, c: float, eps_c: float, seed: int, T: int, client: int,
+                           d_transmit, workspace, stream=None) -> None:
+    """Paper-literal decisions, one per segment of `seg` (host offsets, S + 1
+    of them), into d_transmit (device uint8 [S])."""
+    import torch
+    arr, ptr, S = _seg_array(seg)
+    if d_transmit.numel() != S:
+        raise ValueError("d_transmit needs one entry per segment")
+    rc = load_library().bfasgd_decide_segments(
+        ctypes.byref(state.c), ptr, S, c, eps_c, int(seed) & (2 ** 64 - 1), int(T), int(client),
+        _dev_ptr(d_transmit, torch.uint8, "d_transmit"), _dev_ptr(workspace, torch.uint8, "workspace"),
+        workspace.numel(), _stream(stream))
+    _check(rc)
+
+
+def bfasgd_apply_segments(state: State, grad, seg, d_transmit, client: int, grad_ts: int, stream=None) -> None:
+    """FASGD update on the transmitted segments; T advances by one."""
+    import torch
+    arr, ptr, S = _seg_array(seg)
+    if grad.numel() != state.P:
+        raise ValueError("grad length differs from P")
+    rc = load_library().bfasgd_apply_segments(
+        ctypes.byref(state.c), _dev_ptr(grad, torch.float32, "grad"), ptr, S,
+        _dev_ptr(d_transmit, torch.uint8, "d_transmit"), int(client), int(grad_ts), _stream(stream))
     _check(rc)
 
 

@@ -117,6 +117,34 @@ fasgd_status dense_common(fasgd_state* st, const float* const* grads, const int3
 
 bool finite_nonneg(float x) { return isfinite(x) && x >= 0.0f; }
 
+fasgd_status check_segments(const int64_t* seg, int32_t S, int64_t P)
+{
+    if (!seg) return fail(FASGD_ERR_NULL, "seg is NULL");
+    if (S < 1) return fail(FASGD_ERR_ARG, "S = %d must be >= 1", S);
+    if (seg[0] != 0 || seg[S] != P) return fail(FASGD_ERR_ARG, "segments must start at 0 and end at P");
+    for (int32_t s = 0; s < S; ++s)
+        if (seg[s + 1] <= seg[s]) return fail(FASGD_ERR_ARG, "segment %d is empty or out of order", s);
+    return FASGD_OK;
+}
+
+// Group g0 .. g0 + n - 1 of the segments; partial_base is updated past it.
+fasgd::SegGroup segment_group(const int64_t* seg, int32_t S, int32_t g0, int64_t& partial_base)
+{
+    fasgd::SegGroup g;
+    memset(&g, 0, sizeof g);
+    g.n = S - g0 < fasgd::kSegGroup ? S - g0 : fasgd::kSegGroup;
+    g.first_seg = g0;
+    g.partial_base = partial_base;
+    int64_t blocks = 0;
+    for (int32_t i = 0; i <= g.n; ++i) {
+        g.start[i] = seg[g0 + i];
+        g.block_prefix[i] = blocks;
+        if (i < g.n) blocks += fasgd::seg_blocks(seg[g0 + i + 1] - seg[g0 + i]);
+    }
+    partial_base += blocks;
+    return g;
+}
+
 }  // namespace
 
 extern "C" {
@@ -362,6 +390,78 @@ fasgd_status bfasgd_apply_fetch(float* theta_client, int64_t P, const int32_t* i
         const hipError_t e = fasgd::launch_scatter(theta_client, P, idx, val, d_count, capacity, stream);
         if (e != hipSuccess) return hip_fail(e, "bfasgd_apply_fetch");
     }
+    return ok();
+}
+
+size_t bfasgd_segments_workspace_bytes(int64_t P, int32_t S)
+{
+    if (P < 1 || S < 1) return 0;
+    return fasgd::segments_workspace_bytes(P, S);
+}
+
+fasgd_status bfasgd_decide_segments(const fasgd_state* st, const int64_t* seg, int32_t S, float c, float eps_c,
+                                    uint64_t seed, int64_t T, int32_t client, uint8_t* d_transmit,
+                                    void* workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    if (!st) return fail(FASGD_ERR_NULL, "state is NULL");
+    if (st->P < 1) return fail(FASGD_ERR_ARG, "P must be >= 1");
+    if (st->lambda < 1) return fail(FASGD_ERR_ARG, "lambda = %d must be >= 1", st->lambda);
+    if (!st->v || !d_transmit || !workspace) return fail(FASGD_ERR_NULL, "v, d_transmit or workspace is NULL");
+    fasgd_status s = check_segments(seg, S, st->P);
+    if (s != FASGD_OK) return s;
+    if (!finite_nonneg(c) || !finite_nonneg(eps_c)) return fail(FASGD_ERR_ARG, "c and eps_c must be finite and >= 0");
+    if (T < 0 || T > int64_t(UINT32_MAX)) return fail(FASGD_ERR_ARG, "T = %lld is not in [0, 2^32)", (long long)T);
+    if (client < 0 || client >= st->lambda)
+        return fail(FASGD_ERR_CLIENT, "client = %d is outside [0, %d)", client, st->lambda);
+    if (!aligned(st->v, 4)) return fail(FASGD_ERR_ALIGN, "v is not 4-byte aligned");
+    if (!aligned(workspace, 256)) return fail(FASGD_ERR_ALIGN, "workspace must be 256-byte aligned");
+    if (workspace_bytes < fasgd::segments_workspace_bytes(st->P, S))
+        return fail(FASGD_ERR_CAPACITY, "workspace of %zu bytes is smaller than the %zu needed", workspace_bytes,
+                    fasgd::segments_workspace_bytes(st->P, S));
+    int64_t base = 0;
+    for (int32_t g0 = 0; g0 < S; g0 += fasgd::kSegGroup) {
+        const fasgd::SegGroup g = segment_group(seg, S, g0, base);
+        const hipError_t e = fasgd::launch_seg_decide(g, st->v, static_cast<double*>(workspace), c, eps_c, seed,
+                                                      static_cast<uint32_t>(T), static_cast<uint32_t>(client),
+                                                      d_transmit, stream);
+        if (e != hipSuccess) return hip_fail(e, "bfasgd_decide_segments");
+    }
+    return ok();
+}
+
+fasgd_status bfasgd_apply_segments(fasgd_state* st, const float* grad, const int64_t* seg, int32_t S,
+                                   const uint8_t* d_transmit, int32_t client, int64_t grad_ts, hipStream_t stream)
+{
+    fasgd_status s = check_state(st, true);
+    if (s != FASGD_OK) return s;
+    if (!grad || !d_transmit) return fail(FASGD_ERR_NULL, "grad or d_transmit is NULL");
+    if (!aligned(grad, 4)) return fail(FASGD_ERR_ALIGN, "grad is not 4-byte aligned");
+    s = check_segments(seg, S, st->P);
+    if (s != FASGD_OK) return s;
+    float tau_div;
+    s = staleness(st, &client, &grad_ts, 1, &tau_div);
+    if (s != FASGD_OK) return s;
+    fasgd::SegApplyArgs a;
+    memset(&a, 0, sizeof a);
+    a.theta = st->theta;
+    a.n = st->n;
+    a.b = st->b;
+    a.v = st->v;
+    a.last_T = st->last_T;
+    a.grad = grad;
+    a.transmit = d_transmit;
+    a.coef = st->math_mode == FASGD_MATH_FAST ? st->alpha / tau_div : tau_div;
+    a.last_T_value = static_cast<int32_t>(st->T);
+    a.aligned = aligned(st->theta, 16) && aligned(st->n, 16) && aligned(st->b, 16) && aligned(st->v, 16) &&
+                aligned(st->last_T, 16) && aligned(grad, 16);
+    a.h = hyper_of(st);
+    int64_t base = 0;
+    for (int32_t g0 = 0; g0 < S; g0 += fasgd::kSegGroup) {
+        const fasgd::SegGroup g = segment_group(seg, S, g0, base);
+        const hipError_t e = fasgd::launch_seg_apply(g, a, st->math_mode, stream);
+        if (e != hipSuccess) return hip_fail(e, "bfasgd_apply_segments");
+    }
+    st->T += 1;
     return ok();
 }
 

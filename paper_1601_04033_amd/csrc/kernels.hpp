@@ -79,6 +79,39 @@ struct SparseArgs {
 
 hipError_t launch_sparse(const SparseArgs& a, int mode, hipStream_t s);
 
+// Paper-literal decisions per segment (groups of up to kSegGroup segments).
+constexpr int kSegGroup = 32;
+
+struct SegGroup {
+    int64_t start[kSegGroup + 1];          // offsets of the group's segments, start[n] = end of the last
+    int64_t block_prefix[kSegGroup + 1];   // blocks before segment i within the group
+    int32_t n;                             // segments in the group
+    int32_t pad;
+    int64_t first_seg;                     // global index of the group's first segment
+    int64_t partial_base;                  // partial sums of the group start here
+};
+
+struct SegApplyArgs {
+    float* theta;
+    float* n;
+    float* b;
+    float* v;
+    int32_t* last_T;
+    const float* grad;
+    const uint8_t* transmit;
+    float coef;             // as DenseArgs::coef for this push
+    int32_t last_T_value;   // T
+    int32_t aligned;        // every array 16-byte aligned
+    Hyper h;
+};
+
+int64_t seg_blocks(int64_t length);
+size_t segments_workspace_bytes(int64_t P, int32_t S);
+hipError_t launch_seg_decide(const SegGroup& g, const float* v, double* partial, float c, float eps_c,
+                             uint64_t seed, uint32_t ctr_T, uint32_t ctr_client, uint8_t* transmit,
+                             hipStream_t s);
+hipError_t launch_seg_apply(const SegGroup& g, const SegApplyArgs& a, int mode, hipStream_t s);
+
 // dst[idx[i]] = val[i] for i < min(*d_count, capacity); indices outside
 // [0, P) are skipped.
 hipError_t launch_scatter(float* dst, int64_t P, const int32_t* idx, const float* val,

@@ -227,3 +227,39 @@ def test_next_entry_points_reject_bad_arguments(lib):
     assert fetch(count=None) == 1
     assert fetch(dst=f.ptr(2, misalign=2)) == 5
     assert st.T == 2
+
+
+def test_segment_entry_points_reject_bad_arguments(lib):
+    st, f = _state(P=16, lam=3, T=2)
+    ws_need = fa.bfasgd_segments_workspace_bytes(16, 2)
+    assert ws_need > 0 and fa.bfasgd_segments_workspace_bytes(16, 0) == 0
+    ws = np.zeros(ws_need + 512, np.uint8)
+    wsp = (ws.ctypes.data + 255) & ~255
+    out = np.zeros(8, np.uint8)
+
+    def decide(seg=(0, 5, 16), c=1.0, T=0, client=0, ws_ptr=wsp, ws_bytes=ws_need):
+        a = np.array(seg, np.int64)
+        return lib.bfasgd_decide_segments(ctypes.byref(st), a.ctypes.data, a.size - 1, c, 1e-8, 7, T, client,
+                                          out.ctypes.data, ws_ptr, ws_bytes, None)
+
+    assert decide(seg=(0, 5, 15)) == 2          # does not end at P
+    assert decide(seg=(1, 5, 16)) == 2          # does not start at 0
+    assert decide(seg=(0, 5, 5, 16)) == 2       # empty segment
+    assert decide(seg=(0,)) == 2                # S = 0
+    assert decide(c=-1.0) == 2
+    assert decide(T=2 ** 32) == 2
+    assert decide(client=3) == 4
+    assert decide(ws_bytes=ws_need - 1) == 6
+    assert decide(ws_ptr=wsp + 16) == 5
+    assert lib.bfasgd_decide_segments(ctypes.byref(st), None, 1, 1.0, 0.0, 7, 0, 0, out.ctypes.data, wsp,
+                                      ws_need, None) == 1
+
+    def apply(seg=(0, 5, 16), client=0, ts=0):
+        a = np.array(seg, np.int64)
+        return lib.bfasgd_apply_segments(ctypes.byref(st), f.ptr(5), a.ctypes.data, a.size - 1, out.ctypes.data,
+                                         client, ts, None)
+
+    assert apply(seg=(0, 16, 16)) == 2
+    assert apply(ts=3) == 3
+    assert apply(client=-1) == 4
+    assert st.T == 2

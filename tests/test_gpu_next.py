@@ -112,3 +112,101 @@ def test_fetch_selection_refreshes_client_copy_bit_exact():
     fa.bfasgd_apply_fetch(copy_gpu, idx, val, cnt)
     torch.cuda.synchronize()
     assert torch.equal(copy_gpu, st.theta)
+
+
+# ------------------------------------------------ paper-literal mean-v decision
+def _seg_r(s, seed, T, client):
+    w = oracle.philox4x32_10([s & 0xFFFFFFFF, 0x80000000 | (s >> 32), T & 0xFFFFFFFF, client],
+                             [seed & 0xFFFFFFFF, seed >> 32])[0]
+    return (int(w) >> 8) * 2.0 ** -24
+
+
+def _mlp_segments():
+    offs = [0]
+    for _, n, _ in workload.MLP_LAYOUT:
+        offs.append(offs[-1] + n)
+    return np.array(offs, np.int64)
+
+
+def _check_decisions(got, want, mean, c, seed, T, client, eps_c=1e-8):
+    """Equal, except where the fp64 threshold lies within 1e-12 of r (the two
+    sides sum v in different orders)."""
+    for s in np.flatnonzero(got != want):
+        t = mean[s] + float(np.float32(eps_c))
+        p = t / (t + c)
+        assert abs(_seg_r(int(s), seed, T, client) - p) <= 1e-12 * p, (s, got[s], want[s])
+
+
+@pytest.mark.parametrize("layout", ["whole", "mlp", "many"])
+def test_segment_decisions_match_oracle(layout):
+    import torch
+    dev = gpu()
+    if layout == "mlp":
+        seg = _mlp_segments()
+    elif layout == "whole":
+        seg = np.array([0, 2_000_003], np.int64)
+    else:                                   # 100 segments (four groups), ragged sizes down to 1
+        rng = np.random.default_rng(5)
+        seg = np.unique(np.concatenate([[0, 1, 2, 3, 999_999], rng.integers(4, 999_999, 95), [1_000_000]]))
+        seg = seg.astype(np.int64)
+    P = int(seg[-1])
+    v = workload.synthetic_v(P, seed=P % 1000)
+    st = new_gpu_state(np.zeros(P, np.float32), dev, 16, 0.005, fa.MATH_FAST)
+    st.v.copy_(torch.from_numpy(v))
+    S = seg.size - 1
+    d = torch.zeros(S, device=dev, dtype=torch.uint8)
+    ws = torch.empty(fa.bfasgd_segments_workspace_bytes(P, S), device=dev, dtype=torch.uint8)
+    n_tx = 0
+    for T, client, c in [(0, 0, 30.0), (17, 5, 100.0), (2 ** 32 - 1, 15, 3.0), (9, 2, 0.0)]:
+        fa.bfasgd_decide_segments(st, seg, c, 1e-8, SEED, T, client, d, ws)
+        torch.cuda.synchronize()
+        got = d.cpu().numpy().astype(bool)
+        want, mean = oracle.bfasgd_decide_segments(v, seg, c, 1e-8, SEED, T, client)
+        _check_decisions(got, want, mean, c, SEED, T, client)
+        n_tx += int(got.sum())
+        if c == 0.0:
+            assert got.all()
+        again = [None] * 2
+        for r in range(2):
+            fa.bfasgd_decide_segments(st, seg, c, 1e-8, SEED, T, client, d, ws)
+            torch.cuda.synchronize()
+            again[r] = d.cpu().numpy().astype(bool)
+        assert np.array_equal(again[0], got) and np.array_equal(again[1], got)
+    assert 0 < n_tx
+
+
+@pytest.mark.parametrize("mode", [fa.MATH_FAST, fa.MATH_IEEE])
+def test_mlp_per_tensor_pushes_sequence(mode):
+    """MLP layout, lambda = 16: 16 dense updates, then 200 pushes each decided
+    per tensor from the tensors' mean v and applied on the transmitted
+    tensors only."""
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["mlp_bfasgd"]
+    P = w.P
+    seg = _mlp_segments()
+    S = seg.size - 1
+    theta0, m_, s_ = workload.host_params(w)
+    clients, ts = workload.schedule(w, 216)
+    st = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, mode)
+    ref = oracle.init_state(theta0, alpha=w.alpha_fasgd)
+    warm = [workload.host_gradient(w, m_, s_, k) for k in range(16)]
+    fa.fasgd_apply_updates(st, [to_dev(g, dev) for g in warm], clients[:16], ts[:16])
+    for k in range(16):
+        oracle.fasgd_apply(ref, warm[k], ts[k])
+    c = 3.0 * float(np.mean(ref.v))
+    d = torch.zeros(S, device=dev, dtype=torch.uint8)
+    ws = torch.empty(fa.bfasgd_segments_workspace_bytes(P, S), device=dev, dtype=torch.uint8)
+    sent = 0
+    for t in range(16, 216):
+        g = workload.host_gradient(w, m_, s_, t)
+        fa.bfasgd_decide_segments(st, seg, c, 1e-8, SEED, st.T, clients[t], d, ws)
+        want, mean = oracle.bfasgd_decide_segments(ref.v.astype(np.float32), seg, c, 1e-8, SEED, ref.T, clients[t])
+        fa.bfasgd_apply_segments(st, to_dev(g, dev), seg, d, clients[t], ts[t])
+        oracle.bfasgd_apply_segments(ref, g, seg, want, ts[t])
+        got = d.cpu().numpy().astype(bool)
+        assert np.array_equal(got, want), (t, got, want)
+        sent += int(want.sum())
+    torch.cuda.synchronize()
+    assert_state_close(st, ref, RTOL_SEQ, what="after 200 per-tensor pushes")
+    assert 0 < sent < 200 * S
