@@ -135,7 +135,10 @@ def main():
     cnt = torch.zeros(1, device=dev, dtype=torch.int64)
     ws = fa.allocate_workspace(P, dev)
     per_step = K + 1
-    clients, ts = workload.schedule(w, K + (warm + steps + 4) * per_step)
+    # timestamps used: K (first pass) + (K + 1) per step, then the legs after
+    # the timed region: 3 SASGD passes of K, 3 cached pushes, 3 segment
+    # pushes and 3 synchronous steps
+    clients, ts = workload.schedule(w, K + (warm + steps) * per_step + 3 * K + 9 + 16)
     torch.cuda.synchronize()
 
     ev = {name: [] for name in ("dense", "select", "sparse")}
