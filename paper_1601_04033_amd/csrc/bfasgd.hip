@@ -1,20 +1,32 @@
 // B-FASGD push selection with deterministic ordered compaction, and the
 // sparse server apply of the compacted list.
 //
-// Selection runs in four launches, none of which waits on another block:
-//   mark     one Philox4x32-10 call per 4 parameters (the counter is the
-//            chunk index j/4, so one call feeds one 16-byte vector of v),
-//            four wave ballots per 64 chunks stored to the workspace (1 bit
-//            per parameter), and a per-tile count;
-//   scan     one block per 1024 tiles scans their counts (offsets within
-//            the group) and records the group total;
-//   top      one block scans the group totals and writes the device count;
-//   scatter  every wave rebuilds its output position from the ballots of
-//            its tile (scalar loads and popcounts) plus the group and tile
-//            offsets, stages its (index, value) pairs in LDS and writes its
-//            contiguous piece of the output in ascending index order.
+// Work is cut into wave tiles of kTileSegs segments of 64 chunks (one chunk is
+// 4 consecutive parameters, one 16-byte vector).  Every wave owns one tile and
+// never waits on another wave, so no launch has a block barrier in its
+// streaming part.  Selection runs in three or four launches:
+//   mark     the wave loads its tile of v, draws one Philox4x32-10 call per
+//            chunk (the counter is the chunk index j/4, so one call feeds one
+//            vector of v), forms four ballots per segment (1 bit per
+//            parameter), stores the tile's ballot words in one store and its
+//            transmit count;
+//   scan     one block per 1024 tiles scans their counts (offsets within the
+//            group) and records the group total; the group totals are
+//            scanned and the device count written by the last scan block to
+//            finish or, for many groups, by one more single-block launch;
+//   scatter  the wave loads its tile of gradients, reads its ballot words
+//            (scalar loads), places every transmitted (index, value) pair in
+//            an LDS stage at the popcount of the bits before it (ascending
+//            index order), and writes the staged run at group offset + tile
+//            offset in contiguous stores.
 // The result depends only on (seed, T, client, v, grad), never on timing.
 #include "kernels.hpp"
+
+// v_writelane_b32: write a wave-uniform value into one lane of a VGPR.  The
+// LLVM intrinsic is reached through its symbol name (this compiler has no
+// clang builtin for it), so the backend still schedules it and handles its
+// hazards as for any other instruction.
+__device__ int amdgcn_writelane(int value, int lane, int old) __asm("llvm.amdgcn.writelane.i32");
 
 namespace fasgd {
 namespace {
@@ -22,13 +34,14 @@ namespace {
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
-constexpr int kBlock = 256;                   // 4 waves
-constexpr int kWavesPerBlock = kBlock / kWave;
-constexpr int kItems = 4;                     // 64-chunk segments per wave per tile
-constexpr int kSegsPerTile = kWavesPerBlock * kItems;          // 16
-constexpr int64_t kChunksPerTile = int64_t(kSegsPerTile) * kWave;  // 1024 chunks = 4096 parameters
+constexpr int kSelBlock = 256;                // 4 independent waves
+constexpr int kWavesPerBlock = kSelBlock / kWave;
+constexpr int kTileSegs = 4;                  // 64-chunk segments per wave tile
+constexpr int kTileWords = 4 * kTileSegs;     // ballot words per tile
+constexpr int64_t kChunksPerTile = int64_t(kTileSegs) * kWave;  // 256 chunks = 1024 parameters
 constexpr int kScanBlock = 1024;              // tiles per scan group
-constexpr int kMaxGroups = 4096;              // 2^31 parameters need 512
+constexpr int kMaxGroups = 4096;              // 2^31 parameters need 2048
+constexpr int kFusedTopGroups = 64;           // up to 64 groups: group scan fused into the scan launch
 
 __host__ __device__ inline int64_t n_chunks(int64_t P) { return (P + 3) / 4; }
 int64_t n_tiles(int64_t P) { return (n_chunks(P) + kChunksPerTile - 1) / kChunksPerTile; }
@@ -39,59 +52,79 @@ __device__ __forceinline__ uint64_t lanes_below(int lane)
     return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
-// v for the 4 parameters of chunk q; parameters at or past P read as NaN,
-// which never transmits.
-template <bool ALIGNED>
+// The 4 values of chunk q, one load each; parameters at or past P read as
+// NaN, which never transmits (mark) and is never written (scatter).
 __device__ __forceinline__ f4 load_chunk(const float* p, int64_t q, int64_t P)
 {
     const int64_t j = q * 4;
-    if (ALIGNED && j + 3 < P) return *reinterpret_cast<const f4*>(p + j);
     f4 x;
 #pragma unroll
     for (int c = 0; c < 4; ++c) x[c] = (j + c < P) ? p[j + c] : __builtin_nanf("");
     return x;
 }
 
-template <bool ALIGNED>
-__global__ __launch_bounds__(kBlock) void select_mark(const SelectArgs a)
+// wave tile of this wave (wave-uniform)
+__device__ __forceinline__ int64_t wave_tile()
 {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int64_t tile = blockIdx.x;
+    return static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+}
+
+// Mark one tile.  FULL: the tile lies inside [0, P) and v is 16-byte
+// aligned, so no lane needs a bounds check (every tile but the last).
+template <bool FULL>
+__device__ __forceinline__ void mark_tile(const SelectArgs& a, int64_t tile, int lane)
+{
     const int64_t nch = n_chunks(a.P);
+    const int64_t q0 = tile * kChunksPerTile + lane;
+    // every load of the tile before any arithmetic
+    f4 v[kTileSegs];
+#pragma unroll
+    for (int s = 0; s < kTileSegs; ++s) {
+        const int64_t q = q0 + s * kWave;
+        if (FULL)
+            v[s] = *reinterpret_cast<const f4*>(a.v + q * 4);
+        else if (q < nch)
+            v[s] = load_chunk(a.v, q, a.P);
+    }
+    // lane k < kTileWords holds ballot word k of the tile (low, high halves)
+    int word_lo = 0, word_hi = 0;
     uint32_t count = 0;
 #pragma unroll
-    for (int it = 0; it < kItems; ++it) {
-        const int64_t seg = tile * kSegsPerTile + it * kWavesPerBlock + wave;
-        const int64_t q = seg * kWave + lane;
+    for (int s = 0; s < kTileSegs; ++s) {
+        const int64_t q = q0 + s * kWave;
         uint32_t nib = 0;
-        if (q < nch) {
-            const f4 v = load_chunk<ALIGNED>(a.v, q, a.P);
+        if (FULL || q < nch) {
             const uint4 w = philox4x32_10(
                 make_uint4(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), a.ctr_T, a.ctr_client),
                 a.key0, a.key1);
-            nib = transmit_bit(w.x, v[0], a.c, a.eps_c) | (transmit_bit(w.y, v[1], a.c, a.eps_c) << 1) |
-                  (transmit_bit(w.z, v[2], a.c, a.eps_c) << 2) | (transmit_bit(w.w, v[3], a.c, a.eps_c) << 3);
+            nib = transmit_bit(w.x, v[s][0], a.c, a.eps_c) | (transmit_bit(w.y, v[s][1], a.c, a.eps_c) << 1) |
+                  (transmit_bit(w.z, v[s][2], a.c, a.eps_c) << 2) |
+                  (transmit_bit(w.w, v[s][3], a.c, a.eps_c) << 3);
         }
-        const uint64_t b0 = __builtin_amdgcn_ballot_w64((nib & 1u) != 0);
-        const uint64_t b1 = __builtin_amdgcn_ballot_w64((nib & 2u) != 0);
-        const uint64_t b2 = __builtin_amdgcn_ballot_w64((nib & 4u) != 0);
-        const uint64_t b3 = __builtin_amdgcn_ballot_w64((nib & 8u) != 0);
-        if (lane < 4) {
-            const uint64_t mine = lane == 0 ? b0 : lane == 1 ? b1 : lane == 2 ? b2 : b3;
-            a.ballots[seg * 4 + lane] = mine;
-        }
-        count += __popcll(b0) + __popcll(b1) + __popcll(b2) + __popcll(b3);
-    }
-    __shared__ uint32_t wave_count[kWavesPerBlock];
-    if (lane == 0) wave_count[wave] = count;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint32_t s = 0;
 #pragma unroll
-        for (int w = 0; w < kWavesPerBlock; ++w) s += wave_count[w];
-        a.tile_count[tile] = s;
+        for (int k = 0; k < 4; ++k) {
+            const uint64_t bk = __builtin_amdgcn_ballot_w64(((nib >> k) & 1u) != 0);
+            count += static_cast<uint32_t>(__popcll(bk));
+            word_lo = amdgcn_writelane(static_cast<int>(bk), 4 * s + k, word_lo);
+            word_hi = amdgcn_writelane(static_cast<int>(bk >> 32), 4 * s + k, word_hi);
+        }
     }
+    if (lane < kTileWords)
+        a.ballots[tile * kTileWords + lane] =
+            (static_cast<uint64_t>(static_cast<uint32_t>(word_hi)) << 32) | static_cast<uint32_t>(word_lo);
+    if (lane == 0) a.tile_count[tile] = count;
+}
+
+__global__ __launch_bounds__(kSelBlock) void select_mark(const SelectArgs a, bool aligned)
+{
+    if (blockIdx.x == 0 && threadIdx.x == 0) *a.groups_done = 0u;   // for the scan launch
+    const int64_t tile = wave_tile();
+    if (tile >= a.n_tiles) return;
+    const int lane = threadIdx.x & (kWave - 1);
+    if (aligned && (tile + 1) * kChunksPerTile * 4 <= a.P)
+        mark_tile<true>(a, tile, lane);
+    else
+        mark_tile<false>(a, tile, lane);
 }
 
 // Block-wide exclusive scan of one value per thread (kScanBlock threads).
@@ -122,25 +155,17 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* t
     return inc - x + (wave > 0 ? wave_total[wave - 1] : 0u);
 }
 
-// Group g of 1024 tiles: offsets of its tiles within the group, and its total.
-__global__ __launch_bounds__(kScanBlock) void select_scan(const SelectArgs a)
+// Offsets of the groups (at most kMaxGroups) from their totals, and the
+// number transmitted; run by one block.
+__device__ __forceinline__ void scan_groups(const SelectArgs& a, int64_t ng, bool atomic_loads)
 {
-    const int64_t t = static_cast<int64_t>(blockIdx.x) * kScanBlock + threadIdx.x;
-    const uint32_t c = t < a.n_tiles ? a.tile_count[t] : 0u;
-    uint32_t total;
-    const uint32_t off = block_exclusive_scan(c, &total);
-    if (t < a.n_tiles) a.tile_offset[t] = off;
-    if (threadIdx.x == 0) a.group_total[blockIdx.x] = total;
-}
-
-// Offsets of the groups (at most kMaxGroups) and the number transmitted.
-__global__ __launch_bounds__(kScanBlock) void select_top(const SelectArgs a)
-{
-    const int64_t ng = (a.n_tiles + kScanBlock - 1) / kScanBlock;
     uint32_t carry = 0;
     for (int64_t base = 0; base < ng; base += kScanBlock) {
         const int64_t g = base + threadIdx.x;
-        const uint32_t c = g < ng ? a.group_total[g] : 0u;
+        uint32_t c = 0;
+        if (g < ng)
+            c = atomic_loads ? __hip_atomic_load(a.group_total + g, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT)
+                             : a.group_total[g];
         uint32_t total;
         const uint32_t off = block_exclusive_scan(c, &total);
         if (g < ng) a.group_offset[g] = carry + off;
@@ -150,64 +175,138 @@ __global__ __launch_bounds__(kScanBlock) void select_top(const SelectArgs a)
     if (threadIdx.x == 0) *a.d_count = static_cast<int64_t>(carry);
 }
 
-__device__ __forceinline__ uint32_t seg_count(const uint64_t* b)
+// Group g of 1024 tiles: offsets of its tiles within the group and the group
+// total.  FUSED_TOP: the last group block to arrive (arrival counter, zeroed
+// by the mark launch before this one) then scans the group totals itself.
+// Each arrival is a device-scope release, which costs more than a launch once
+// there are many groups; then select_top does that scan as its own launch.
+template <bool FUSED_TOP>
+__global__ __launch_bounds__(kScanBlock) void select_scan(const SelectArgs a)
 {
-    return static_cast<uint32_t>(__popcll(b[0]) + __popcll(b[1]) + __popcll(b[2]) + __popcll(b[3]));
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * kScanBlock + threadIdx.x;
+    const uint32_t c = t < a.n_tiles ? a.tile_count[t] : 0u;
+    uint32_t total;
+    const uint32_t off = block_exclusive_scan(c, &total);
+    if (t < a.n_tiles) a.tile_offset[t] = off;
+    if (!FUSED_TOP) {
+        if (threadIdx.x == 0) a.group_total[blockIdx.x] = total;
+        return;
+    }
+    __shared__ bool last;
+    if (threadIdx.x == 0) {
+        __hip_atomic_store(a.group_total + blockIdx.x, total, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        // release: the total is visible before the arrival is counted
+        const uint32_t before = __hip_atomic_fetch_add(a.groups_done, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+        last = before == gridDim.x - 1;
+    }
+    __syncthreads();
+    if (last) scan_groups(a, gridDim.x, true);
 }
 
-template <bool ALIGNED>
-__global__ __launch_bounds__(kBlock) void select_scatter(const SelectArgs a)
+__global__ __launch_bounds__(kScanBlock) void select_top(const SelectArgs a)
 {
-    __shared__ int32_t s_idx[kWavesPerBlock][4 * kWave];
-    __shared__ float s_val[kWavesPerBlock][4 * kWave];
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int64_t tile = blockIdx.x;
-    const uint64_t below = lanes_below(lane);
-    const uint64_t* tb = a.ballots + tile * kSegsPerTile * 4;
+    scan_groups(a, (a.n_tiles + kScanBlock - 1) / kScanBlock, false);
+}
 
-    // output position of segment (0, wave): group and tile offsets plus
-    // everything the earlier segments of this tile transmitted
-    int64_t seg_base = static_cast<int64_t>(a.group_offset[tile / kScanBlock]) + a.tile_offset[tile];
-    for (int s = 0; s < wave; ++s) seg_base += seg_count(tb + 4 * s);
+// Scatter one tile; FULL as for mark_tile.  The tile's entries are staged
+// in output order in the wave's LDS slice and leave in contiguous full-wave
+// stores (a lane storing its own entries directly issues four sparse masked
+// stores per segment).  The slice holds kStageEntries; a segment that would
+// overflow it flushes it first, so the slice stays small enough for full
+// occupancy while a tile at any transmit fraction up to about 1/4 leaves in
+// one flush.
+constexpr int kStageEntries = 4 * kWave;     // one segment's worth
 
-#pragma unroll
-    for (int it = 0; it < kItems; ++it) {
-        const int s = it * kWavesPerBlock + wave;
-        const uint64_t b0 = tb[4 * s], b1 = tb[4 * s + 1], b2 = tb[4 * s + 2], b3 = tb[4 * s + 3];
-        const uint32_t n_seg = static_cast<uint32_t>(__popcll(b0) + __popcll(b1) + __popcll(b2) + __popcll(b3));
-        const uint32_t nib = static_cast<uint32_t>((b0 >> lane) & 1) | static_cast<uint32_t>(((b1 >> lane) & 1) << 1) |
-                             static_cast<uint32_t>(((b2 >> lane) & 1) << 2) |
-                             static_cast<uint32_t>(((b3 >> lane) & 1) << 3);
-        if (nib) {
-            uint32_t p = static_cast<uint32_t>(__popcll(b0 & below) + __popcll(b1 & below) + __popcll(b2 & below) +
-                                               __popcll(b3 & below));
-            const int64_t q = (tile * kSegsPerTile + s) * kWave + lane;
-            const f4 g = load_chunk<ALIGNED>(a.grad, q, a.P);
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                if ((nib >> c) & 1u) {
-                    s_idx[wave][p] = static_cast<int32_t>(q * 4 + c);
-                    s_val[wave][p] = g[c];
-                    ++p;
-                }
-            }
+__device__ __forceinline__ void wave_lds_order()
+{
+    // the wave's LDS operations execute in order; keep the compiler from
+    // moving the reads of other lanes' entries above the writes
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// entries [0, n) of the stage to output positions [base, base + n)
+__device__ __forceinline__ void drain(const SelectArgs& a, const int32_t* s_idx, const float* s_val, uint32_t n,
+                                      int64_t base, int lane)
+{
+    for (uint32_t e = lane; e < n; e += kWave) {
+        const int64_t pos = base + e;
+        if (pos < a.capacity) {
+            a.out_idx[pos] = s_idx[e];
+            a.out_val[pos] = s_val[e];
         }
-        __syncthreads();
-        // the segment's n_seg entries are contiguous in the output
-        for (uint32_t e = lane; e < n_seg; e += kWave) {
-            const int64_t pos = seg_base + e;
-            if (pos < a.capacity) {
-                a.out_idx[pos] = s_idx[wave][e];
-                a.out_val[pos] = s_val[wave][e];
-            }
-        }
-        __syncthreads();
-        // advance past this segment and the other waves' segments of this item
-        for (int t = s; t < s + kWavesPerBlock && t < kSegsPerTile; ++t) seg_base += seg_count(tb + 4 * t);
     }
 }
 
+template <bool FULL>
+__device__ __forceinline__ void scatter_tile(const SelectArgs& a, int64_t tile, int lane, int32_t* s_idx,
+                                             float* s_val)
+{
+    const int64_t nch = n_chunks(a.P);
+    const int64_t q0 = tile * kChunksPerTile + lane;
+    // every gradient load of the tile first (at any transmit fraction worth
+    // compacting every line holds a transmitted value, so this costs no traffic)
+    f4 g[kTileSegs];
+#pragma unroll
+    for (int s = 0; s < kTileSegs; ++s) {
+        const int64_t q = q0 + s * kWave;
+        if (FULL)
+            g[s] = *reinterpret_cast<const f4*>(a.grad + q * 4);
+        else if (q < nch)
+            g[s] = load_chunk(a.grad, q, a.P);
+    }
+    const uint64_t* tb = a.ballots + tile * kTileWords;
+    const uint64_t below = lanes_below(lane);
+    int64_t base = static_cast<int64_t>(a.group_offset[tile / kScanBlock]) + a.tile_offset[tile];
+    uint32_t staged = 0;
+#pragma unroll
+    for (int s = 0; s < kTileSegs; ++s) {
+        const uint64_t b0 = tb[4 * s], b1 = tb[4 * s + 1], b2 = tb[4 * s + 2], b3 = tb[4 * s + 3];
+        const uint32_t nib = static_cast<uint32_t>((b0 >> lane) & 1) | static_cast<uint32_t>(((b1 >> lane) & 1) << 1) |
+                             static_cast<uint32_t>(((b2 >> lane) & 1) << 2) |
+                             static_cast<uint32_t>(((b3 >> lane) & 1) << 3);
+        const uint32_t n_seg = __popcll(b0) + __popcll(b1) + __popcll(b2) + __popcll(b3);
+        if (staged + n_seg > static_cast<uint32_t>(kStageEntries)) {
+            wave_lds_order();
+            drain(a, s_idx, s_val, staged, base, lane);
+            wave_lds_order();
+            base += staged;
+            staged = 0;
+        }
+        // entries of the lanes below come first; within a lane, ascending c
+        uint32_t p = staged + __popcll(b0 & below) + __popcll(b1 & below) + __popcll(b2 & below) +
+                     __popcll(b3 & below);
+        const int64_t q = q0 + s * kWave;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            if ((nib >> c) & 1u) {
+                s_idx[p] = static_cast<int32_t>(q * 4 + c);
+                s_val[p] = g[s][c];
+                ++p;
+            }
+        }
+        staged += n_seg;
+    }
+    wave_lds_order();
+    drain(a, s_idx, s_val, staged, base, lane);
+}
+
+__global__ __launch_bounds__(kSelBlock) void select_scatter(const SelectArgs a, bool aligned)
+{
+    __shared__ int32_t s_idx[kWavesPerBlock][kStageEntries];
+    __shared__ float s_val[kWavesPerBlock][kStageEntries];
+    const int64_t tile = wave_tile();
+    if (tile >= a.n_tiles) return;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int w = threadIdx.x / kWave;
+    if (aligned && (tile + 1) * kChunksPerTile * 4 <= a.P)
+        scatter_tile<true>(a, tile, lane, s_idx[w], s_val[w]);
+    else
+        scatter_tile<false>(a, tile, lane, s_idx[w], s_val[w]);
+}
+
+constexpr int kListBlock = 256;               // list kernels: 4 waves
 constexpr int kSparseE = 2;                   // list entries per lane
 constexpr int64_t kListMaxBlocks = 65536;     // grid cap of the list kernels (grid-stride)
 
@@ -216,14 +315,14 @@ constexpr int64_t kListMaxBlocks = 65536;     // grid cap of the list kernels (g
 // (ascending indices, so few cache lines), and each thread issues all 4 E of
 // its gathers before the first update.
 template <int MODE>
-__global__ __launch_bounds__(kBlock) void sparse_apply(const SparseArgs a)
+__global__ __launch_bounds__(kListBlock) void sparse_apply(const SparseArgs a)
 {
     int64_t m = *a.d_count;
     if (m > a.capacity) m = a.capacity;
     const Hyper h = a.h;
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t wave_id = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / kWave;
-    const int64_t n_waves = static_cast<int64_t>(gridDim.x) * (kBlock / kWave);
+    const int64_t wave_id = (static_cast<int64_t>(blockIdx.x) * kListBlock + threadIdx.x) / kWave;
+    const int64_t n_waves = static_cast<int64_t>(gridDim.x) * (kListBlock / kWave);
     for (int64_t base = wave_id * kWave * kSparseE; base < m; base += n_waves * kWave * kSparseE) {
         int64_t j[kSparseE];
         float g[kSparseE], th[kSparseE], n[kSparseE], b[kSparseE], v[kSparseE];
@@ -251,15 +350,15 @@ __global__ __launch_bounds__(kBlock) void sparse_apply(const SparseArgs a)
     }
 }
 
-__global__ __launch_bounds__(kBlock) void scatter_list(float* __restrict__ dst, int64_t P,
+__global__ __launch_bounds__(kListBlock) void scatter_list(float* __restrict__ dst, int64_t P,
                                                        const int32_t* __restrict__ idx,
                                                        const float* __restrict__ val,
                                                        const int64_t* __restrict__ d_count, int64_t capacity)
 {
     int64_t m = *d_count;
     if (m > capacity) m = capacity;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < m; i += stride) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kListBlock;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kListBlock + threadIdx.x; i < m; i += stride) {
         const int64_t j = idx[i];
         if (j >= 0 && j < P) dst[j] = val[i];
     }
@@ -270,8 +369,8 @@ __global__ __launch_bounds__(kBlock) void scatter_list(float* __restrict__ dst, 
 size_t select_workspace_bytes(int64_t P)
 {
     const int64_t nt = n_tiles(P);
-    return align256(size_t(nt) * kSegsPerTile * 4 * sizeof(uint64_t)) + 2 * align256(size_t(nt) * sizeof(uint32_t)) +
-           2 * align256(size_t(kMaxGroups) * sizeof(uint32_t));
+    return align256(size_t(nt) * kTileWords * sizeof(uint64_t)) + 2 * align256(size_t(nt) * sizeof(uint32_t)) +
+           2 * align256(size_t(kMaxGroups) * sizeof(uint32_t)) + align256(sizeof(uint32_t));
 }
 
 void select_workspace_layout(void* ws, int64_t P, SelectArgs& a)
@@ -279,7 +378,7 @@ void select_workspace_layout(void* ws, int64_t P, SelectArgs& a)
     const int64_t nt = n_tiles(P);
     char* p = static_cast<char*>(ws);
     a.ballots = reinterpret_cast<uint64_t*>(p);
-    p += align256(size_t(nt) * kSegsPerTile * 4 * sizeof(uint64_t));
+    p += align256(size_t(nt) * kTileWords * sizeof(uint64_t));
     a.tile_count = reinterpret_cast<uint32_t*>(p);
     p += align256(size_t(nt) * sizeof(uint32_t));
     a.tile_offset = reinterpret_cast<uint32_t*>(p);
@@ -287,30 +386,30 @@ void select_workspace_layout(void* ws, int64_t P, SelectArgs& a)
     a.group_total = reinterpret_cast<uint32_t*>(p);
     p += align256(size_t(kMaxGroups) * sizeof(uint32_t));
     a.group_offset = reinterpret_cast<uint32_t*>(p);
+    p += align256(size_t(kMaxGroups) * sizeof(uint32_t));
+    a.groups_done = reinterpret_cast<uint32_t*>(p);
     a.n_tiles = nt;
 }
 
 hipError_t launch_select(const SelectArgs& a, bool aligned, hipStream_t s)
 {
-    const unsigned grid = static_cast<unsigned>(a.n_tiles);
+    const unsigned grid = static_cast<unsigned>((a.n_tiles + kWavesPerBlock - 1) / kWavesPerBlock);
     const unsigned groups = static_cast<unsigned>((a.n_tiles + kScanBlock - 1) / kScanBlock);
     if (groups > static_cast<unsigned>(kMaxGroups)) return hipErrorInvalidValue;
-    if (aligned)
-        select_mark<true><<<grid, kBlock, 0, s>>>(a);
-    else
-        select_mark<false><<<grid, kBlock, 0, s>>>(a);
+    select_mark<<<grid, kSelBlock, 0, s>>>(a, aligned);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    select_scan<<<groups, kScanBlock, 0, s>>>(a);
+    if (groups <= static_cast<unsigned>(kFusedTopGroups)) {
+        select_scan<true><<<groups, kScanBlock, 0, s>>>(a);
+    } else {
+        select_scan<false><<<groups, kScanBlock, 0, s>>>(a);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        select_top<<<1, kScanBlock, 0, s>>>(a);
+    }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    select_top<<<1, kScanBlock, 0, s>>>(a);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    if (aligned)
-        select_scatter<true><<<grid, kBlock, 0, s>>>(a);
-    else
-        select_scatter<false><<<grid, kBlock, 0, s>>>(a);
+    select_scatter<<<grid, kSelBlock, 0, s>>>(a, aligned);
     return hipGetLastError();
 }
 
@@ -318,23 +417,23 @@ hipError_t launch_sparse(const SparseArgs& a, int mode, hipStream_t s)
 {
     // enough lanes for `capacity` entries (the count is only known on the
     // device); lanes past the count exit
-    int64_t g = (a.capacity + int64_t(kBlock) * kSparseE - 1) / (int64_t(kBlock) * kSparseE);
+    int64_t g = (a.capacity + int64_t(kListBlock) * kSparseE - 1) / (int64_t(kListBlock) * kSparseE);
     if (g > kListMaxBlocks) g = kListMaxBlocks;
     if (g < 1) g = 1;
     if (mode == MATH_FAST)
-        sparse_apply<MATH_FAST><<<static_cast<unsigned>(g), kBlock, 0, s>>>(a);
+        sparse_apply<MATH_FAST><<<static_cast<unsigned>(g), kListBlock, 0, s>>>(a);
     else
-        sparse_apply<MATH_IEEE><<<static_cast<unsigned>(g), kBlock, 0, s>>>(a);
+        sparse_apply<MATH_IEEE><<<static_cast<unsigned>(g), kListBlock, 0, s>>>(a);
     return hipGetLastError();
 }
 
 hipError_t launch_scatter(float* dst, int64_t P, const int32_t* idx, const float* val,
                           const int64_t* d_count, int64_t capacity, hipStream_t s)
 {
-    int64_t g = (capacity + kBlock - 1) / kBlock;
+    int64_t g = (capacity + kListBlock - 1) / kListBlock;
     if (g > kListMaxBlocks) g = kListMaxBlocks;
     if (g < 1) g = 1;
-    scatter_list<<<static_cast<unsigned>(g), kBlock, 0, s>>>(dst, P, idx, val, d_count, capacity);
+    scatter_list<<<static_cast<unsigned>(g), kListBlock, 0, s>>>(dst, P, idx, val, d_count, capacity);
     return hipGetLastError();
 }
 

@@ -50,14 +50,20 @@ __device__ __forceinline__ void fasgd_step(float& th, float& n, float& b, float&
 // words 1 and 3 and the round key, become the new words 0 and 2, the low
 // halves the new words 3 and 1.  The key steps by the Weyl increments
 // between rounds.  The key is uniform across a wave and stays in SGPRs.
+// Each three-way xor is one v_bitop3_b32 (truth table 0x96) on gfx950.
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c)
+{
+    return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
+
 __device__ __forceinline__ uint4 philox4x32_10(uint4 x, uint32_t k0, uint32_t k1)
 {
 #pragma unroll
     for (int i = 0; i < 10; ++i) {
         const uint64_t m0 = static_cast<uint64_t>(x.x) * 0xD2511F53ull;
         const uint64_t m2 = static_cast<uint64_t>(x.z) * 0xCD9E8D57ull;
-        x = make_uint4(static_cast<uint32_t>(m2 >> 32) ^ x.y ^ k0, static_cast<uint32_t>(m2),
-                       static_cast<uint32_t>(m0 >> 32) ^ x.w ^ k1, static_cast<uint32_t>(m0));
+        x = make_uint4(xor3(static_cast<uint32_t>(m2 >> 32), x.y, k0), static_cast<uint32_t>(m2),
+                       xor3(static_cast<uint32_t>(m0 >> 32), x.w, k1), static_cast<uint32_t>(m0));
         k0 += 0x9E3779B9u;
         k1 += 0xBB67AE85u;
     }

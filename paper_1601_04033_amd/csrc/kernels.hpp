@@ -46,6 +46,7 @@ struct SelectArgs {
     uint32_t* tile_offset;   // within its group of 1024 tiles
     uint32_t* group_total;
     uint32_t* group_offset;
+    uint32_t* groups_done;  // arrival counter of the scan blocks
     int64_t P;
     int64_t capacity;
     int64_t n_tiles;
