@@ -138,7 +138,9 @@ def main():
     # timestamps used: K (first pass) + (K + 1) per step, then the legs after
     # the timed region: 3 SASGD passes of K, 3 cached pushes, 3 segment
     # pushes and 3 synchronous steps
-    clients, ts = workload.schedule(w, K + (warm + steps) * per_step + 3 * K + 9 + 16)
+    # and the dense passes at K = 1, 8, 32 (11 calls each)
+    KS = (1, 8, 32)
+    clients, ts = workload.schedule(w, K + (warm + steps) * per_step + 3 * K + 9 + 16 + 11 * sum(KS))
     torch.cuda.synchronize()
 
     ev = {name: [] for name in ("dense", "select", "sparse")}
@@ -207,6 +209,35 @@ def main():
         sas_ms.append(a.elapsed_time(b_))
     sas_ms_avg = float(np.mean(sas_ms[1:]))
     sas_bytes = P * (8 + 4 * K)
+
+    def batch_ms(fn, n):
+        """Per-call ms of n back-to-back calls between two events (after one
+        untimed call): the rate the kernels sustain, without per-call event
+        and dispatch gaps."""
+        fn()
+        a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(n):
+            fn()
+        b_.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b_) / n
+
+    # the push selection back to back on the step's last inputs
+    sel_b2b_ms = batch_ms(lambda: fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, st.T, clients[st.T],
+                                                          idx, val, cnt, ws), 20)
+    m_b2b = int(cnt.item())
+    sel_b2b_bytes = P * 8 + m_b2b * 8
+    # the dense pass at K = 1, 8, 32 (gradients fused per pass), back to back
+    dense_k = {}
+    for k in KS:
+        def dense_pass(k=k):
+            base = st.T
+            fa.fasgd_apply_updates(st, pool[:k], clients[base:base + k], ts[base:base + k])
+        kms = batch_ms(dense_pass, 10)
+        dense_k[str(k)] = {"ms": kms, "GB/s": P * (32 + 4 * k) / (kms * 1e-3) / 1e9,
+                           "frac": P * (32 + 4 * k) / (kms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                           "param_updates_per_s": P * k / (kms * 1e-3)}
 
     def timed(fn, reps=3):
         out = []
@@ -282,8 +313,12 @@ def main():
                      "traffic": traffic, "algorithmic_bytes": dense_bytes},
         "kernels": {
             "fasgd_apply_updates": {"ms": dense_ms, "GB/s": achieved,
-                                    "param_updates_per_s": P * K / (dense_ms * 1e-3)},
+                                    "param_updates_per_s": P * K / (dense_ms * 1e-3),
+                                    "back_to_back_by_K": dense_k},
             "bfasgd_select_compact": {"ms": sel_ms, "GB/s": sel_bytes / (sel_ms * 1e-3) / 1e9,
+                                      "ms_back_to_back": sel_b2b_ms,
+                                      "GB/s_back_to_back": sel_b2b_bytes / (sel_b2b_ms * 1e-3) / 1e9,
+                                      "frac_back_to_back": sel_b2b_bytes / (sel_b2b_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
                                       "transmitted_fraction": m_avg / P},
             "bfasgd_apply_sparse": {"ms": sp_ms, "GB/s_algorithmic": sp_bytes / (sp_ms * 1e-3) / 1e9},
             "sasgd_apply_updates": {"ms": sas_ms_avg, "GB/s": sas_bytes / (sas_ms_avg * 1e-3) / 1e9},
