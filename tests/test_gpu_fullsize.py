@@ -172,3 +172,31 @@ def test_dense_beyond_int32_parameters():
     assert_state_close(st, ref, RTOL_SEQ, js=jt, what="P > 2^31")
     del grads, sg, st, m, s
     _free()
+
+
+@pytest.mark.parametrize("P", [64 * 1024 * 1024, 64 * 1024 * 1024 + 1])
+def test_select_at_group_scan_switch(P):
+    """Selection is bit-exact on both sides of the switch between the fused
+    group scan (at most 64 groups of 1024 tiles of 1024 parameters) and the
+    separate single-block group scan (65 groups and more)."""
+    import torch
+    dev = gpu()
+    v = workload.synthetic_v(P, seed=11)
+    g = np.random.default_rng(12).standard_normal(P).astype(np.float32)
+    st = new_gpu_state(np.zeros(P, np.float32), dev, 16, 0.005, fa.MATH_FAST)
+    st.v.copy_(torch.from_numpy(v))
+    gd = torch.from_numpy(g).to(dev)
+    idx = torch.empty(P, device=dev, dtype=torch.int32)
+    val = torch.empty(P, device=dev)
+    cnt = torch.zeros(1, device=dev, dtype=torch.int64)
+    ws = fa.allocate_workspace(P, dev)
+    c = 40.0
+    fa.bfasgd_select_compact(st, gd, c, 1e-8, SEED, 9, 5, idx, val, cnt, ws)
+    torch.cuda.synchronize()
+    m = int(cnt.item())
+    r_idx, r_val, r_m = oracle.bfasgd_select(v, g, c, 1e-8, SEED, 9, 5)
+    assert m == r_m
+    np.testing.assert_array_equal(idx[:m].cpu().numpy(), r_idx)
+    np.testing.assert_array_equal(val[:m].cpu().numpy().view(np.uint32), r_val.view(np.uint32))
+    del st, gd, idx, val, cnt, ws
+    _free()
