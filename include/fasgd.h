@@ -51,8 +51,18 @@ typedef enum fasgd_status {
 
 typedef enum fasgd_math {
     FASGD_MATH_IEEE = 0,        /* correctly rounded fp32 sqrt and divisions */
-    FASGD_MATH_FAST = 1         /* hardware reciprocal square root and reciprocal (about 1 ulp each) */
+    FASGD_MATH_FAST = 1         /* hardware (reciprocal) square root and reciprocal (about 1 ulp each) */
 } fasgd_math;
+
+/*
+ * Which moving average v keeps (Sec. 2.2).  The equation for v averages
+ * 1/sqrt(n - b^2 + eps); the text around it describes a moving average of
+ * the standard deviation.  The rate is alpha / (v tau) in both.
+ */
+typedef enum fasgd_v_reading {
+    FASGD_V_EQUATIONS = 0,      /* v <- beta v + (1 - beta) / sqrt(n - b^2 + eps)   (default) */
+    FASGD_V_PROSE = 1           /* v <- beta v + (1 - beta) * sqrt(n - b^2 + eps) */
+} fasgd_v_reading;
 
 /*
  * Server state (Sec. 2.2).  A host-side POD owned by the caller; the device
@@ -60,7 +70,8 @@ typedef enum fasgd_math {
  *   theta   parameters theta, fp32 [P]
  *   n       moving average of the squared gradient, fp32 [P]
  *   b       moving average of the gradient, fp32 [P]
- *   v       moving average of 1/sqrt(n - b^2 + eps), fp32 [P]
+ *   v       moving average of 1/sqrt(n - b^2 + eps) (or, with
+ *           v_reading = FASGD_V_PROSE, of sqrt(n - b^2 + eps)), fp32 [P]
  *   last_T  timestamp of the last sparse (B-FASGD) update of each
  *           parameter, int32 [P], -1 before the first
  * Per-parameter staleness bookkeeping: a dense apply updates every
@@ -81,7 +92,7 @@ typedef struct fasgd_state {
     float beta;
     float eps;
     int32_t math_mode;          /* fasgd_math */
-    int32_t reserved;           /* 0 */
+    int32_t v_reading;          /* fasgd_v_reading; fasgd_init_state sets FASGD_V_EQUATIONS */
     int64_t T;
     int64_t dense_T;            /* timestamp of the last dense update, -1 before the first */
     float* theta;
@@ -97,7 +108,9 @@ typedef struct fasgd_state {
  * T = 0 (Sec. 2.1) and dense_T = -1, and records the hyper-parameters in
  * *st.  theta must already hold the initial parameters; it is not written.
  * Requires P >= 1, lambda >= 1, mu >= 1, alpha > 0, gamma and beta in
- * [0, 1], eps > 0 (finite), math_mode a fasgd_math value.
+ * [0, 1], eps > 0 (finite), math_mode a fasgd_math value.  v_reading is set
+ * to FASGD_V_EQUATIONS; a caller may set it to FASGD_V_PROSE before the
+ * first update (the apply calls reject other values with FASGD_ERR_ARG).
  * n, b, v may be NULL for a state used only with sasgd_apply_updates.
  */
 fasgd_status fasgd_init_state(fasgd_state* st, int64_t P, int32_t lambda, int32_t mu,

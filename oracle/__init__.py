@@ -33,7 +33,7 @@ def _load():
     d, f, i64, i32, u64 = ctypes.c_double, ctypes.c_float, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64
     lib.oracle_philox4x32_10.argtypes = [u32p, u32p, u32p]
     lib.oracle_philox4x32_10.restype = None
-    lib.oracle_fasgd_apply.argtypes = [i64, dp, dp, dp, dp, i64p, i64p, fp, i64, d, d, d, d]
+    lib.oracle_fasgd_apply.argtypes = [i64, dp, dp, dp, dp, i64p, i64p, fp, i64, d, d, d, d, i32]
     lib.oracle_fasgd_apply.restype = ctypes.c_int
     lib.oracle_sasgd_apply.argtypes = [i64, dp, i64p, i64p, fp, i64, d]
     lib.oracle_sasgd_apply.restype = ctypes.c_int
@@ -43,15 +43,15 @@ def _load():
     lib.oracle_bfasgd_decide.restype = None
     lib.oracle_bfasgd_select.argtypes = [i64, fp, fp, f, f, u64, i64, i32, i32p, fp, i64]
     lib.oracle_bfasgd_select.restype = ctypes.c_int64
-    lib.oracle_bfasgd_apply_sparse.argtypes = [dp, dp, dp, dp, i64p, i64p, i32p, fp, i64, i64, d, d, d, d]
+    lib.oracle_bfasgd_apply_sparse.argtypes = [dp, dp, dp, dp, i64p, i64p, i32p, fp, i64, i64, d, d, d, d, i32]
     lib.oracle_bfasgd_apply_sparse.restype = ctypes.c_int
     lib.oracle_sync_sgd_apply.argtypes = [i64, dp, i64p, i64p, P(fp), i32, d]
     lib.oracle_sync_sgd_apply.restype = None
-    lib.oracle_bfasgd_apply_cached.argtypes = [i64, dp, dp, dp, dp, i64p, i64p, fp, i32p, fp, i64, i64, d, d, d, d]
+    lib.oracle_bfasgd_apply_cached.argtypes = [i64, dp, dp, dp, dp, i64p, i64p, fp, i32p, fp, i64, i64, d, d, d, d, i32]
     lib.oracle_bfasgd_apply_cached.restype = ctypes.c_int
     lib.oracle_bfasgd_decide_segments.argtypes = [i64, i64p, fp, f, f, u64, i64, i32, u8p, dp]
     lib.oracle_bfasgd_decide_segments.restype = None
-    lib.oracle_bfasgd_apply_segments.argtypes = [i64, i64p, u8p, dp, dp, dp, dp, i64p, i64p, fp, i64, d, d, d, d]
+    lib.oracle_bfasgd_apply_segments.argtypes = [i64, i64p, u8p, dp, dp, dp, dp, i64p, i64p, fp, i64, d, d, d, d, i32]
     lib.oracle_bfasgd_apply_segments.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -102,15 +102,19 @@ class State:
                      self.v[js].copy(), self.last_T[js].copy(), self.T, dict(self.hyper))
 
 
-def init_state(theta0, alpha, gamma=0.95, beta=0.9, eps=1e-4, n0=0.0, b0=0.0, v0=0.0) -> State:
+def init_state(theta0, alpha, gamma=0.95, beta=0.9, eps=1e-4, n0=0.0, b0=0.0, v0=0.0, v_reading=0) -> State:
     """Server initialisation: theta from theta0 (fp32 values), n, b, v constant,
-    last_T = -1, T = 0 (the timestamp starts at 0, Sec. 2.1)."""
+    last_T = -1, T = 0 (the timestamp starts at 0, Sec. 2.1).  v_reading 0: v
+    follows the equation for v (average of 1/sqrt(n - b^2 + eps)); 1: v is
+    the moving average of the standard deviation the text describes."""
     theta0 = np.asarray(theta0)
     P = theta0.shape[0]
     st = State(theta=theta0.astype(np.float32).astype(np.float64),
                n=np.full(P, f32(n0)), b=np.full(P, f32(b0)), v=np.full(P, f32(v0)),
                last_T=np.full(P, -1, dtype=np.int64), T=0)
-    st.hyper = dict(alpha=f32(alpha), gamma=f32(gamma), beta=f32(beta), eps=f32(eps))
+    if v_reading not in (0, 1):
+        raise OracleError("v_reading must be 0 or 1")
+    st.hyper = dict(alpha=f32(alpha), gamma=f32(gamma), beta=f32(beta), eps=f32(eps), reading=int(v_reading))
     return st
 
 
@@ -126,7 +130,7 @@ def fasgd_apply(st: State, grad, grad_ts: int) -> None:
                                 _ptr(st.b, ctypes.c_double), _ptr(st.v, ctypes.c_double),
                                 _ptr(st.last_T, ctypes.c_int64), ctypes.byref(T),
                                 _ptr(grad, ctypes.c_float), int(grad_ts),
-                                h["alpha"], h["gamma"], h["beta"], h["eps"])
+                                h["alpha"], h["gamma"], h["beta"], h["eps"], h.get("reading", 0))
     if rc != 0:
         raise OracleError(f"negative staleness: grad_ts={grad_ts} > T={st.T}")
     st.T = T.value
@@ -203,7 +207,7 @@ def bfasgd_apply_sparse(st: State, idx, val, grad_ts: int) -> None:
                                         _ptr(st.b, ctypes.c_double), _ptr(st.v, ctypes.c_double),
                                         _ptr(st.last_T, ctypes.c_int64), ctypes.byref(T),
                                         _ptr(idx, ctypes.c_int32), _ptr(val, ctypes.c_float), idx.shape[0],
-                                        int(grad_ts), h["alpha"], h["gamma"], h["beta"], h["eps"])
+                                        int(grad_ts), h["alpha"], h["gamma"], h["beta"], h["eps"], h.get("reading", 0))
     if rc != 0:
         raise OracleError(f"negative staleness: grad_ts={grad_ts} > T={st.T}")
     st.T = T.value
@@ -245,7 +249,7 @@ def bfasgd_apply_cached(st: State, cache, idx, val, grad_ts: int) -> None:
                                         _ptr(st.last_T, ctypes.c_int64), ctypes.byref(T),
                                         _ptr(cache, ctypes.c_float), _ptr(idx, ctypes.c_int32),
                                         _ptr(val, ctypes.c_float), idx.shape[0], int(grad_ts),
-                                        h["alpha"], h["gamma"], h["beta"], h["eps"])
+                                        h["alpha"], h["gamma"], h["beta"], h["eps"], h.get("reading", 0))
     if rc != 0:
         raise OracleError(f"negative staleness: grad_ts={grad_ts} > T={st.T}")
     st.T = T.value
@@ -289,7 +293,7 @@ def bfasgd_apply_segments(st: State, grad, seg, transmit, grad_ts: int) -> None:
                                           _ptr(st.b, ctypes.c_double), _ptr(st.v, ctypes.c_double),
                                           _ptr(st.last_T, ctypes.c_int64), ctypes.byref(T),
                                           _ptr(grad, ctypes.c_float), int(grad_ts),
-                                          h["alpha"], h["gamma"], h["beta"], h["eps"])
+                                          h["alpha"], h["gamma"], h["beta"], h["eps"], h.get("reading", 0))
     if rc != 0:
         raise OracleError(f"negative staleness: grad_ts={grad_ts} > T={st.T}")
     st.T = T.value

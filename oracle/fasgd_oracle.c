@@ -15,6 +15,8 @@
  *   tau    step-staleness i - j of a gradient with timestamp j    (Sec. 2.1)
  *   n, b   moving averages of the squared gradient and gradient   (Sec. 2.2, eqs. for n_i, b_i)
  *   v      moving average of 1/sqrt(n - b^2 + eps)                (Sec. 2.2, eq. for v_i)
+ *          or, in the prose reading (reading = 1), of sqrt(n - b^2 + eps), the
+ *          moving average of the standard deviation the text of Sec. 2.2 describes
  *   step   alpha / (v * tau) * grad, theta <- theta - step         (Sec. 2.2, FASGD update rule)
  *
  * Readings where the paper is silent (each listed in the design notes):
@@ -67,7 +69,7 @@ void oracle_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t
 /* ------------------------------------------------------------------------- */
 static void fasgd_update_one(double *theta, double *n, double *b, double *v, double g,
                              double alpha, double gamma, double beta, double eps,
-                             double tau_div)
+                             double tau_div, int reading)
 {
     /* n_i = gamma n_{i-1} + (1 - gamma) (grad)^2, elementwise */
     *n = gamma * (*n) + (1.0 - gamma) * g * g;
@@ -77,7 +79,10 @@ static void fasgd_update_one(double *theta, double *n, double *b, double *v, dou
     double var = *n - (*b) * (*b);
     if (var < 0.0)
         var = 0.0;
-    *v = beta * (*v) + (1.0 - beta) / sqrt(var + eps);
+    if (reading == 0)
+        *v = beta * (*v) + (1.0 - beta) / sqrt(var + eps);
+    else /* v averages the standard deviation sqrt(n_i - b_i^2 + eps) */
+        *v = beta * (*v) + (1.0 - beta) * sqrt(var + eps);
     /* g_i = alpha / (v_i tau) * grad ;  theta_{i+1} = theta_i - g_i */
     double step = alpha / ((*v) * tau_div) * g;
     *theta = *theta - step;
@@ -97,18 +102,19 @@ static int staleness_divisor(int64_t T, int64_t grad_ts, double *tau_div)
  * FASGD server apply-update for one client gradient (the lock serialises
  * arrivals, so several gradients are several calls in arrival order).
  * theta, n, b, v: fp64 [P]; last_T: int64 [P] or NULL; *T is advanced by one.
+ * reading: 0 = v as in the equation for v_i, 1 = v as the text describes it.
  * Returns 0, or -1 if grad_ts is not in [0, *T] (negative staleness).
  */
 int oracle_fasgd_apply(int64_t P, double *theta, double *n, double *b, double *v,
                        int64_t *last_T, int64_t *T, const float *grad, int64_t grad_ts,
-                       double alpha, double gamma, double beta, double eps)
+                       double alpha, double gamma, double beta, double eps, int reading)
 {
     double tau_div;
     if (staleness_divisor(*T, grad_ts, &tau_div) != 0)
         return -1;
     for (int64_t j = 0; j < P; ++j) {
         fasgd_update_one(&theta[j], &n[j], &b[j], &v[j], (double)grad[j],
-                         alpha, gamma, beta, eps, tau_div);
+                         alpha, gamma, beta, eps, tau_div, reading);
         if (last_T)
             last_T[j] = *T;
     }
@@ -199,7 +205,7 @@ int64_t oracle_bfasgd_select(int64_t P, const float *v, const float *grad, float
 int oracle_bfasgd_apply_sparse(double *theta, double *n, double *b, double *v, int64_t *last_T,
                                int64_t *T, const int32_t *idx, const float *val, int64_t m,
                                int64_t grad_ts, double alpha, double gamma, double beta,
-                               double eps)
+                               double eps, int reading)
 {
     double tau_div;
     if (staleness_divisor(*T, grad_ts, &tau_div) != 0)
@@ -207,7 +213,7 @@ int oracle_bfasgd_apply_sparse(double *theta, double *n, double *b, double *v, i
     for (int64_t i = 0; i < m; ++i) {
         int64_t j = idx[i];
         fasgd_update_one(&theta[j], &n[j], &b[j], &v[j], (double)val[i],
-                         alpha, gamma, beta, eps, tau_div);
+                         alpha, gamma, beta, eps, tau_div, reading);
         if (last_T)
             last_T[j] = *T;
     }
@@ -245,11 +251,12 @@ void oracle_sync_sgd_apply(int64_t P, double *theta, int64_t *last_T, int64_t *T
 int oracle_bfasgd_apply_cached(int64_t P, double *theta, double *n, double *b, double *v,
                                int64_t *last_T, int64_t *T, float *cache, const int32_t *idx,
                                const float *val, int64_t m, int64_t grad_ts, double alpha,
-                               double gamma, double beta, double eps)
+                               double gamma, double beta, double eps, int reading)
 {
     for (int64_t i = 0; i < m; ++i)
         cache[idx[i]] = val[i];
-    return oracle_fasgd_apply(P, theta, n, b, v, last_T, T, cache, grad_ts, alpha, gamma, beta, eps);
+    return oracle_fasgd_apply(P, theta, n, b, v, last_T, T, cache, grad_ts, alpha, gamma, beta, eps,
+                              reading);
 }
 
 /* ------------------------------------------------------------------------- */
@@ -291,7 +298,7 @@ void oracle_bfasgd_decide_segments(int64_t S, const int64_t *seg, const float *v
 int oracle_bfasgd_apply_segments(int64_t S, const int64_t *seg, const uint8_t *transmit,
                                  double *theta, double *n, double *b, double *v, int64_t *last_T,
                                  int64_t *T, const float *grad, int64_t grad_ts, double alpha,
-                                 double gamma, double beta, double eps)
+                                 double gamma, double beta, double eps, int reading)
 {
     double tau_div;
     if (staleness_divisor(*T, grad_ts, &tau_div) != 0)
@@ -301,7 +308,7 @@ int oracle_bfasgd_apply_segments(int64_t S, const int64_t *seg, const uint8_t *t
             continue;
         for (int64_t j = seg[s]; j < seg[s + 1]; ++j) {
             fasgd_update_one(&theta[j], &n[j], &b[j], &v[j], (double)grad[j],
-                             alpha, gamma, beta, eps, tau_div);
+                             alpha, gamma, beta, eps, tau_div, reading);
             if (last_T)
                 last_T[j] = *T;
         }

@@ -24,6 +24,8 @@ LIB_PATH = os.path.join(_HERE, "libfasgd.so")
 FASGD_MAX_K = 64
 MATH_IEEE = 0
 MATH_FAST = 1
+V_EQUATIONS = 0     # v averages 1/sqrt(n - b^2 + eps) (Sec. 2.2's equation)
+V_PROSE = 1         # v averages sqrt(n - b^2 + eps) (Sec. 2.2's text)
 
 STATUS = {0: "FASGD_OK", 1: "FASGD_ERR_NULL", 2: "FASGD_ERR_ARG", 3: "FASGD_ERR_STALENESS",
           4: "FASGD_ERR_CLIENT", 5: "FASGD_ERR_ALIGN", 6: "FASGD_ERR_CAPACITY", 7: "FASGD_ERR_HIP"}
@@ -46,7 +48,7 @@ class fasgd_state(ctypes.Structure):
     """Mirror of the C struct fasgd_state."""
     _fields_ = [("P", ctypes.c_int64), ("lambda_", ctypes.c_int32), ("mu", ctypes.c_int32),
                 ("alpha", ctypes.c_float), ("gamma", ctypes.c_float), ("beta", ctypes.c_float),
-                ("eps", ctypes.c_float), ("math_mode", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("eps", ctypes.c_float), ("math_mode", ctypes.c_int32), ("v_reading", ctypes.c_int32),
                 ("T", ctypes.c_int64), ("dense_T", ctypes.c_int64),
                 ("theta", ctypes.c_void_p), ("n", ctypes.c_void_p), ("b", ctypes.c_void_p),
                 ("v", ctypes.c_void_p), ("last_T", ctypes.c_void_p)]
@@ -154,8 +156,10 @@ class State:
 def fasgd_init_state(theta, n, b, v, last_T, *, lam: int, mu: int = 1, alpha: float,
                      gamma: float = 0.95, beta: float = 0.9, eps: float = 1e-4,
                      math_mode: int = MATH_FAST, n0: float = 0.0, b0: float = 0.0, v0: float = 0.0,
-                     stream=None) -> State:
-    """theta (holding theta0), n, b, v: fp32 [P]; last_T: int32 [P].  n, b, v may be None (SASGD only)."""
+                     v_reading: int = V_EQUATIONS, stream=None) -> State:
+    """theta (holding theta0), n, b, v: fp32 [P]; last_T: int32 [P].  n, b, v may be None (SASGD only).
+    v_reading selects which average v keeps (V_EQUATIONS or V_PROSE); it is a
+    field of the state that the apply calls validate."""
     import torch
     P = theta.numel()
     for name, t in (("n", n), ("b", b), ("v", v), ("last_T", last_T)):
@@ -168,6 +172,7 @@ def fasgd_init_state(theta, n, b, v, last_T, *, lam: int, mu: int = 1, alpha: fl
         _dev_ptr(b, torch.float32, "b", True), _dev_ptr(v, torch.float32, "v", True),
         _dev_ptr(last_T, torch.int32, "last_T"), _stream(stream))
     _check(rc)
+    st.v_reading = v_reading
     return State(st, dict(theta=theta, n=n, b=b, v=v, last_T=last_T))
 
 

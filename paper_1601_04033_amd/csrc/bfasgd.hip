@@ -413,17 +413,21 @@ hipError_t launch_select(const SelectArgs& a, bool aligned, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t launch_sparse(const SparseArgs& a, int mode, hipStream_t s)
+hipError_t launch_sparse(const SparseArgs& a, int variant, hipStream_t s)
 {
     // enough lanes for `capacity` entries (the count is only known on the
     // device); lanes past the count exit
     int64_t g = (a.capacity + int64_t(kListBlock) * kSparseE - 1) / (int64_t(kListBlock) * kSparseE);
     if (g > kListMaxBlocks) g = kListMaxBlocks;
     if (g < 1) g = 1;
-    if (mode == MATH_FAST)
-        sparse_apply<MATH_FAST><<<static_cast<unsigned>(g), kListBlock, 0, s>>>(a);
-    else
-        sparse_apply<MATH_IEEE><<<static_cast<unsigned>(g), kListBlock, 0, s>>>(a);
+    const unsigned grid = static_cast<unsigned>(g);
+    switch (variant) {
+    case kernel_variant(MATH_FAST, 0): sparse_apply<kernel_variant(MATH_FAST, 0)><<<grid, kListBlock, 0, s>>>(a); break;
+    case kernel_variant(MATH_IEEE, 0): sparse_apply<kernel_variant(MATH_IEEE, 0)><<<grid, kListBlock, 0, s>>>(a); break;
+    case kernel_variant(MATH_FAST, 1): sparse_apply<kernel_variant(MATH_FAST, 1)><<<grid, kListBlock, 0, s>>>(a); break;
+    case kernel_variant(MATH_IEEE, 1): sparse_apply<kernel_variant(MATH_IEEE, 1)><<<grid, kListBlock, 0, s>>>(a); break;
+    default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 

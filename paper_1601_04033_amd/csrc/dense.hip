@@ -214,20 +214,25 @@ hipError_t launch_init(float* n, float* b, float* v, int32_t* last_T, int64_t P,
     return hipGetLastError();
 }
 
-hipError_t launch_fasgd_dense(const DenseArgs& a, int mode, bool aligned, hipStream_t s)
+template <int VARIANT>
+void launch_dense_variant(const DenseArgs& a, bool aligned, unsigned grid, hipStream_t s)
+{
+    if (aligned)
+        fasgd_dense_vec<VARIANT><<<grid, kBlock, 0, s>>>(a);
+    else
+        fasgd_dense_scalar<VARIANT><<<grid, kBlock, 0, s>>>(a);
+}
+
+hipError_t launch_fasgd_dense(const DenseArgs& a, int variant, bool aligned, hipStream_t s)
 {
     // vector path: nvec chunks plus one thread for the tail
     const unsigned grid = aligned ? grid_for((a.P >> 2) + 1) : grid_for(a.P);
-    if (aligned) {
-        if (mode == MATH_FAST)
-            fasgd_dense_vec<MATH_FAST><<<grid, kBlock, 0, s>>>(a);
-        else
-            fasgd_dense_vec<MATH_IEEE><<<grid, kBlock, 0, s>>>(a);
-    } else {
-        if (mode == MATH_FAST)
-            fasgd_dense_scalar<MATH_FAST><<<grid, kBlock, 0, s>>>(a);
-        else
-            fasgd_dense_scalar<MATH_IEEE><<<grid, kBlock, 0, s>>>(a);
+    switch (variant) {
+    case kernel_variant(MATH_FAST, 0): launch_dense_variant<kernel_variant(MATH_FAST, 0)>(a, aligned, grid, s); break;
+    case kernel_variant(MATH_IEEE, 0): launch_dense_variant<kernel_variant(MATH_IEEE, 0)>(a, aligned, grid, s); break;
+    case kernel_variant(MATH_FAST, 1): launch_dense_variant<kernel_variant(MATH_FAST, 1)>(a, aligned, grid, s); break;
+    case kernel_variant(MATH_IEEE, 1): launch_dense_variant<kernel_variant(MATH_IEEE, 1)>(a, aligned, grid, s); break;
+    default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }

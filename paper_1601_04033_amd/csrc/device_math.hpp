@@ -8,6 +8,13 @@
 namespace fasgd {
 
 enum : int { MATH_IEEE = 0, MATH_FAST = 1 };
+// Which v the update keeps (bit 1 of a kernel variant; bit 0 is the math mode):
+//   V_EQUATIONS  v averages 1/sqrt(n - b^2 + eps), Sec. 2.2's equation for v;
+//   V_PROSE      v averages sqrt(n - b^2 + eps), the moving average of the
+//                standard deviation that Sec. 2.2's text describes.
+// Both divide the rate by v.
+enum : int { V_EQUATIONS = 0, V_PROSE = 2 };
+constexpr int kernel_variant(int math_mode, int v_reading) { return math_mode | (v_reading ? V_PROSE : 0); }
 
 // Scalars of one weight update that are the same for every parameter.
 struct Hyper {
@@ -21,26 +28,31 @@ struct Hyper {
 
 // One parameter, one gradient: the FASGD update of Sec. 2.2.
 //   n <- gamma n + (1-gamma) g^2 ; b <- gamma b + (1-gamma) g
-//   v <- beta v + (1-beta) / sqrt(max(n - b^2, 0) + eps)
+//   v <- beta v + (1-beta) / sqrt(max(n - b^2, 0) + eps)     (V_EQUATIONS)
+//   v <- beta v + (1-beta) * sqrt(max(n - b^2, 0) + eps)     (V_PROSE)
 //   theta <- theta - alpha / (v tau) g
-// `coef` carries the staleness: tau (as float) in IEEE mode, and the
-// precomputed alpha / tau in FAST mode (so that the only per-parameter
-// division becomes one hardware reciprocal).
-template <int MODE>
+// VARIANT = math mode | v reading.  `coef` carries the staleness: tau (as
+// float) in IEEE mode, and the precomputed alpha / tau in FAST mode (so
+// that the only per-parameter division becomes one hardware reciprocal).
+template <int VARIANT>
 __device__ __forceinline__ void fasgd_step(float& th, float& n, float& b, float& v, float g,
                                            float coef, const Hyper& h)
 {
+    constexpr bool fast = (VARIANT & MATH_FAST) != 0;
+    constexpr bool prose = (VARIANT & V_PROSE) != 0;
     const float a = h.omg * g;                 // (1 - gamma) g
     n = fmaf(h.gamma, n, a * g);
     b = fmaf(h.gamma, b, a);
     float var = fmaf(-b, b, n);                // n - b^2, one rounding
     var = fmaxf(var, 0.0f);
     const float x = var + h.eps;
-    if constexpr (MODE == MATH_FAST) {
-        v = fmaf(h.beta, v, h.omb * __builtin_amdgcn_rsqf(x));
+    if constexpr (fast) {
+        const float s = prose ? __builtin_amdgcn_sqrtf(x) : __builtin_amdgcn_rsqf(x);
+        v = fmaf(h.beta, v, h.omb * s);
         th = fmaf(-(coef * __builtin_amdgcn_rcpf(v)), g, th);
     } else {
-        v = fmaf(h.beta, v, h.omb * (1.0f / sqrtf(x)));
+        const float s = prose ? sqrtf(x) : 1.0f / sqrtf(x);
+        v = fmaf(h.beta, v, h.omb * s);
         th = fmaf(-(h.alpha / (v * coef)), g, th);
     }
 }

@@ -51,7 +51,15 @@ fasgd_status check_state(const fasgd_state* st, bool need_stats)
         return fail(FASGD_ERR_ALIGN, "state arrays must be 4-byte aligned");
     if (need_stats && st->math_mode != FASGD_MATH_IEEE && st->math_mode != FASGD_MATH_FAST)
         return fail(FASGD_ERR_ARG, "math_mode = %d is not a fasgd_math value", st->math_mode);
+    if (need_stats && st->v_reading != FASGD_V_EQUATIONS && st->v_reading != FASGD_V_PROSE)
+        return fail(FASGD_ERR_ARG, "v_reading = %d is not a fasgd_v_reading value", st->v_reading);
     return FASGD_OK;
+}
+
+// kernel template variant of a validated state
+int variant_of(const fasgd_state* st)
+{
+    return fasgd::kernel_variant(st->math_mode, st->v_reading == FASGD_V_PROSE);
 }
 
 fasgd::Hyper hyper_of(const fasgd_state* st)
@@ -180,6 +188,7 @@ fasgd_status fasgd_init_state(fasgd_state* st, int64_t P, int32_t lambda, int32_
     s.beta = beta;
     s.eps = eps;
     s.math_mode = math_mode;
+    s.v_reading = FASGD_V_EQUATIONS;
     s.T = 0;
     s.dense_T = -1;
     s.theta = theta;
@@ -198,7 +207,7 @@ fasgd_status fasgd_apply_updates(fasgd_state* st, const float* const* grads, con
     bool vec = false;
     fasgd_status s = dense_common(st, grads, clients, grad_ts, K, true, a, vec);
     if (s != FASGD_OK) return s;
-    const hipError_t e = fasgd::launch_fasgd_dense(a, st->math_mode, vec, stream);
+    const hipError_t e = fasgd::launch_fasgd_dense(a, variant_of(st), vec, stream);
     if (e != hipSuccess) return hip_fail(e, "fasgd_apply_updates");
     st->dense_T = st->T + K - 1;
     st->T += K;
@@ -297,7 +306,7 @@ fasgd_status bfasgd_apply_sparse(fasgd_state* st, const int32_t* idx, const floa
     a.last_T_value = static_cast<int32_t>(st->T);
     a.h = hyper_of(st);
     if (capacity > 0) {
-        const hipError_t e = fasgd::launch_sparse(a, st->math_mode, stream);
+        const hipError_t e = fasgd::launch_sparse(a, variant_of(st), stream);
         if (e != hipSuccess) return hip_fail(e, "bfasgd_apply_sparse");
     }
     st->T += 1;
@@ -370,7 +379,7 @@ fasgd_status bfasgd_apply_cached(fasgd_state* st, const int32_t* idx, const floa
     a.h = hyper_of(st);
     const bool vec = aligned(st->theta, 16) && aligned(st->n, 16) && aligned(st->b, 16) && aligned(st->v, 16) &&
                      aligned(cache, 16);
-    const hipError_t e = fasgd::launch_fasgd_dense(a, st->math_mode, vec, stream);
+    const hipError_t e = fasgd::launch_fasgd_dense(a, variant_of(st), vec, stream);
     if (e != hipSuccess) return hip_fail(e, "bfasgd_apply_cached");
     st->dense_T = st->T;
     st->T += 1;
@@ -458,7 +467,7 @@ fasgd_status bfasgd_apply_segments(fasgd_state* st, const float* grad, const int
     int64_t base = 0;
     for (int32_t g0 = 0; g0 < S; g0 += fasgd::kSegGroup) {
         const fasgd::SegGroup g = segment_group(seg, S, g0, base);
-        const hipError_t e = fasgd::launch_seg_apply(g, a, st->math_mode, stream);
+        const hipError_t e = fasgd::launch_seg_apply(g, a, variant_of(st), stream);
         if (e != hipSuccess) return hip_fail(e, "bfasgd_apply_segments");
     }
     st->T += 1;

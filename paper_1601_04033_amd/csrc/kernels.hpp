@@ -28,7 +28,8 @@ struct DenseArgs {
 
 hipError_t launch_init(float* n, float* b, float* v, int32_t* last_T, int64_t P,
                        float n0, float b0, float v0, hipStream_t s);
-hipError_t launch_fasgd_dense(const DenseArgs& a, int mode, bool aligned, hipStream_t s);
+// variant: kernel_variant(math mode, v reading)
+hipError_t launch_fasgd_dense(const DenseArgs& a, int variant, bool aligned, hipStream_t s);
 hipError_t launch_sasgd_dense(const DenseArgs& a, bool aligned, hipStream_t s);
 // theta <- theta - coef[k] * (g_k / lambda), k in order (coef[k] = lr)
 hipError_t launch_sync_sgd(const DenseArgs& a, bool aligned, hipStream_t s);
@@ -78,7 +79,7 @@ struct SparseArgs {
     Hyper h;
 };
 
-hipError_t launch_sparse(const SparseArgs& a, int mode, hipStream_t s);
+hipError_t launch_sparse(const SparseArgs& a, int variant, hipStream_t s);
 
 // Paper-literal decisions per segment (groups of up to kSegGroup segments).
 constexpr int kSegGroup = 32;
@@ -111,7 +112,7 @@ size_t segments_workspace_bytes(int64_t P, int32_t S);
 hipError_t launch_seg_decide(const SegGroup& g, const float* v, double* partial, float c, float eps_c,
                              uint64_t seed, uint32_t ctr_T, uint32_t ctr_client, uint8_t* transmit,
                              hipStream_t s);
-hipError_t launch_seg_apply(const SegGroup& g, const SegApplyArgs& a, int mode, hipStream_t s);
+hipError_t launch_seg_apply(const SegGroup& g, const SegApplyArgs& a, int variant, hipStream_t s);
 
 // dst[idx[i]] = val[i] for i < min(*d_count, capacity); indices outside
 // [0, P) are skipped.

@@ -153,13 +153,16 @@ hipError_t launch_seg_decide(const SegGroup& g, const float* v, double* partial,
     return hipGetLastError();
 }
 
-hipError_t launch_seg_apply(const SegGroup& g, const SegApplyArgs& a, int mode, hipStream_t s)
+hipError_t launch_seg_apply(const SegGroup& g, const SegApplyArgs& a, int variant, hipStream_t s)
 {
     const unsigned blocks = static_cast<unsigned>(g.block_prefix[g.n]);
-    if (mode == MATH_FAST)
-        seg_apply<MATH_FAST><<<blocks, kThreads, 0, s>>>(g, a);
-    else
-        seg_apply<MATH_IEEE><<<blocks, kThreads, 0, s>>>(g, a);
+    switch (variant) {
+    case kernel_variant(MATH_FAST, 0): seg_apply<kernel_variant(MATH_FAST, 0)><<<blocks, kThreads, 0, s>>>(g, a); break;
+    case kernel_variant(MATH_IEEE, 0): seg_apply<kernel_variant(MATH_IEEE, 0)><<<blocks, kThreads, 0, s>>>(g, a); break;
+    case kernel_variant(MATH_FAST, 1): seg_apply<kernel_variant(MATH_FAST, 1)><<<blocks, kThreads, 0, s>>>(g, a); break;
+    case kernel_variant(MATH_IEEE, 1): seg_apply<kernel_variant(MATH_IEEE, 1)><<<blocks, kThreads, 0, s>>>(g, a); break;
+    default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 

@@ -52,7 +52,8 @@ def assert_state_close(st_gpu, ref, rtol, js=None, what=""):
     assert st_gpu.T == ref.T
 
 
-def new_gpu_state(theta0, dev, lam, alpha, mode, gamma=0.95, beta=0.9, eps=1e-4, v0=0.0, sasgd=False):
+def new_gpu_state(theta0, dev, lam, alpha, mode, gamma=0.95, beta=0.9, eps=1e-4, v0=0.0, sasgd=False,
+                  v_reading=0):
     import torch
     P = theta0.shape[0] if hasattr(theta0, "shape") else theta0.numel()
     theta, n, b, v, last_T = fa.allocate_state(P, dev, with_stats=not sasgd)
@@ -61,7 +62,7 @@ def new_gpu_state(theta0, dev, lam, alpha, mode, gamma=0.95, beta=0.9, eps=1e-4,
     else:
         theta.copy_(theta0)
     return fa.fasgd_init_state(theta, n, b, v, last_T, lam=lam, alpha=alpha, gamma=gamma, beta=beta,
-                               eps=eps, math_mode=mode, v0=v0)
+                               eps=eps, math_mode=mode, v0=v0, v_reading=v_reading)
 
 
 def sample_indices(P, k=4096, seed=0):

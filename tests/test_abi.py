@@ -122,6 +122,20 @@ def test_dense_rejects_bad_arguments(lib, fn):
     assert st.T == 3
 
 
+def test_v_reading_validated_by_fasgd_not_by_sasgd(lib):
+    """v_reading must be a fasgd_v_reading value for the updates that keep v;
+    SASGD never reads v, so it does not look at the field."""
+    st, f = _state(T=1)
+    assert st.v_reading == fa.V_EQUATIONS
+    st.v_reading = 2
+    assert _call_dense(lib, "fasgd_apply_updates", st, [0], fake=f) == 2
+    assert b"v_reading" in lib.fasgd_last_error()
+    st.v_reading = -1
+    assert _call_dense(lib, "fasgd_apply_updates", st, [0], fake=f) == 2
+    assert _call_dense(lib, "sasgd_apply_updates", st, [7], fake=f) == 3   # reaches the staleness check
+    assert st.T == 1
+
+
 def test_fasgd_needs_statistics_but_sasgd_does_not_validate_them(lib):
     st, f = _state(T=1)
     st.n = None

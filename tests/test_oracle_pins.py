@@ -130,19 +130,21 @@ def test_sasgd_divides_by_step_staleness():
                                rtol=1e-15, atol=1e-16)
 
 
-def test_fasgd_with_frozen_v_is_sasgd_and_sgd():
-    """beta = 1 and v0 = 1 keep v = 1, so FASGD's rate alpha/(v tau) is SASGD's
-    alpha/tau; with one client (tau = 0) both are plain SGD."""
+@pytest.mark.parametrize("reading", [0, 1])
+def test_fasgd_with_frozen_v_is_sasgd_and_sgd(reading):
+    """beta = 1 and v0 = 1 keep v = 1 (in either reading of v), so FASGD's
+    rate alpha/(v tau) is SASGD's alpha/tau; with one client (tau = 0) both
+    are plain SGD."""
     theta0, grads = _random_problem()
     alpha = oracle.f32(0.005)
-    a = oracle.init_state(theta0, alpha=alpha, beta=1.0, v0=1.0)
+    a = oracle.init_state(theta0, alpha=alpha, beta=1.0, v0=1.0, v_reading=reading)
     for t, g in enumerate(grads):
         oracle.fasgd_apply(a, g, grad_ts=t)
     assert (a.v == 1.0).all()
     ref = _torch_sgd(theta0, grads, [alpha] * len(grads))
     np.testing.assert_allclose(a.theta, ref, rtol=1e-14, atol=1e-17)
     # staleness > 0: torch SGD with rate alpha / tau
-    b = oracle.init_state(theta0, alpha=alpha, beta=1.0, v0=1.0)
+    b = oracle.init_state(theta0, alpha=alpha, beta=1.0, v0=1.0, v_reading=reading)
     ts = [0, 0, 1, 0, 2, 5, 3, 7, 8, 1, 10, 4]
     lrs = []
     for t, (g, j) in enumerate(zip(grads, ts)):
@@ -152,15 +154,19 @@ def test_fasgd_with_frozen_v_is_sasgd_and_sgd():
 
 
 # -------------------------------------------------------------- closed forms
+@pytest.mark.parametrize("reading", [0, 1])
 @pytest.mark.parametrize("gamma,beta,eps", [(0.95, 0.9, 1e-4), (0.5, 0.25, 1e-8), (0.0, 0.9, 1e-4)])
-def test_constant_gradient_closed_form(gamma, beta, eps):
+def test_constant_gradient_closed_form(gamma, beta, eps, reading):
     """For a constant gradient g from n0 = b0 = 0: n_i = (1 - gamma^i) g^2,
     b_i = (1 - gamma^i) g and n_i - b_i^2 = gamma^i (1 - gamma^i) g^2; v_i is
-    the beta-weighted sum of 1/sqrt(that + eps); theta moves by alpha g/(v_i tau_i)."""
+    the beta-weighted sum of 1/sqrt(that + eps) (reading 0, the equation for
+    v) or of sqrt(that + eps) (reading 1, the standard deviation of the text);
+    theta moves by alpha g/(v_i tau_i)."""
     gamma, beta, eps = oracle.f32(gamma), oracle.f32(beta), oracle.f32(eps)
     gs = np.array([0.3, -1.25, 2e-3, 7.0], dtype=np.float32)
     alpha = oracle.f32(0.01)
-    st = oracle.init_state(np.zeros(4, np.float32), alpha=alpha, gamma=gamma, beta=beta, eps=eps)
+    st = oracle.init_state(np.zeros(4, np.float32), alpha=alpha, gamma=gamma, beta=beta, eps=eps,
+                           v_reading=reading)
     g = gs.astype(np.float64)
     v_ref = np.zeros(4)
     theta_ref = np.zeros(4)
@@ -172,13 +178,51 @@ def test_constant_gradient_closed_form(gamma, beta, eps):
         np.testing.assert_allclose(st.n, w * g * g, rtol=1e-13)
         np.testing.assert_allclose(st.b, w * g, rtol=1e-13)
         d = gamma ** i * w * g * g
-        v_ref = beta * v_ref + (1 - beta) / np.sqrt(d + eps)
+        s_ref = np.sqrt(d + eps) if reading else 1.0 / np.sqrt(d + eps)
+        v_ref = beta * v_ref + (1 - beta) * s_ref
         theta_ref = theta_ref - alpha * g / (v_ref * max(tau, 1))
         # n - b^2 is a cancellation: its fp64 error is a few ulp of n, which
         # is large relative to n - b^2 + eps when eps and gamma^i are tiny.
         cond = 1e-12 + 8 * 2.0 ** -52 * st.n / (d + eps)
         assert (np.abs(st.v - v_ref) <= cond * v_ref).all(), (i, st.v, v_ref)
         np.testing.assert_allclose(st.theta, theta_ref, rtol=i * cond.max(), atol=1e-18)
+
+
+def test_prose_v_gamma0_closed_form():
+    """Reading 1 with gamma = 0 and a constant gradient: n = g^2 and b = g
+    after every update, so n - b^2 = 0 and v_i = (1 - beta^i) sqrt(eps)
+    exactly as a geometric sum; theta_I = theta_0 - sum_i alpha g / v_i."""
+    beta, eps, alpha = oracle.f32(0.75), oracle.f32(1e-4), oracle.f32(0.02)
+    gs = np.array([0.5, -2.0, 1e-3, 3.0, 0.0], dtype=np.float32)
+    st = oracle.init_state(np.zeros(5, np.float32), alpha=alpha, gamma=0.0, beta=beta, eps=eps, v_reading=1)
+    theta_ref = np.zeros(5)
+    for i in range(1, 31):
+        oracle.fasgd_apply(st, gs, grad_ts=st.T)          # tau = 0: divisor 1
+        v_i = (1.0 - beta ** i) * np.sqrt(eps)
+        np.testing.assert_allclose(st.v, np.full(5, v_i), rtol=1e-14)
+        theta_ref = theta_ref - alpha * gs.astype(np.float64) / v_i
+        np.testing.assert_allclose(st.theta, theta_ref, rtol=1e-13, atol=1e-300)
+
+
+def test_readings_reciprocal_at_beta0():
+    """With beta = 0 each reading's v is its own term: 1/sqrt(n - b^2 + eps)
+    for the equation and sqrt(n - b^2 + eps) for the text, so after every
+    update the two states' v multiply to 1, and n, b (which v does not feed)
+    agree exactly."""
+    theta0, grads = _random_problem()
+    a = oracle.init_state(theta0, alpha=0.01, beta=0.0, v_reading=0)
+    b = oracle.init_state(theta0, alpha=0.01, beta=0.0, v_reading=1)
+    for t, g in enumerate(grads):
+        oracle.fasgd_apply(a, g, grad_ts=max(t - 2, 0))
+        oracle.fasgd_apply(b, g, grad_ts=max(t - 2, 0))
+        np.testing.assert_array_equal(a.n, b.n)
+        np.testing.assert_array_equal(a.b, b.b)
+        np.testing.assert_allclose(a.v * b.v, 1.0, rtol=4e-16)
+
+
+def test_v_reading_rejected_unless_0_or_1():
+    with pytest.raises(oracle.OracleError):
+        oracle.init_state(np.zeros(3, np.float32), alpha=0.01, v_reading=2)
 
 
 # ------------------------------------------------------ metamorphic relations
