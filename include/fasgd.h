@@ -78,6 +78,11 @@ typedef enum fasgd_v_reading {
  * parameter, so it records its timestamp once in dense_T instead of
  * writing P copies of it; the last update that touched parameter j is
  * max(last_T[j], dense_T) (-1: never updated).
+ * index_base: a state may hold the slice [index_base, index_base + P) of a
+ * larger parameter vector (one shard of a server split by index range).  The
+ * updates are elementwise and ignore it; B-FASGD decisions draw their random
+ * word from the global index index_base + j, so they do not depend on how the
+ * vector is split.  fasgd_init_state sets 0.
  * Hyper-parameters: alpha (Sec. 2.1), gamma, beta, eps (Sec. 2.2).
  * lambda bounds the client ids; mu is recorded only (a gradient arrives as
  * the minibatch mean, Sec. 2.2).  T and dense_T are advanced by the apply
@@ -100,6 +105,8 @@ typedef struct fasgd_state {
     float* b;
     float* v;
     int32_t* last_T;
+    int64_t index_base;         /* global index of parameter 0 (a multiple of 4); 0 unless this
+                                   state is one slice of a larger vector */
 } fasgd_state;
 
 /*
@@ -158,12 +165,14 @@ size_t bfasgd_workspace_bytes(int64_t P);
  * the per-parameter direction of Sec. 5).  Parameter j of this push is
  * transmitted iff r_j < 1 / (1 + c / (v_j + eps_c)), decided in fp32 as
  *   t = v_j + eps_c,  u = t + c,  transmit <=> r_j * u - t < 0 (one rounding),
- * where r_j is the top 24 bits of word (j mod 4) of Philox4x32-10 at counter
- * (j/4 low 32 bits, j/4 high 32 bits, T, client) with key (seed low, seed
- * high), scaled by 2^-24 into [0, 1).  v is read from the state as it is
- * before this push is applied.
+ * where r_j is the top 24 bits of word (J mod 4) of Philox4x32-10 at counter
+ * (J/4 low 32 bits, J/4 high 32 bits, T, client) with key (seed low, seed
+ * high), scaled by 2^-24 into [0, 1), and J = st->index_base + j is the
+ * global index (index_base must be a multiple of 4, >= 0, with
+ * index_base + P <= 2^62; otherwise FASGD_ERR_ARG).  v is read from the
+ * state as it is before this push is applied.
  * The transmitted entries are written in ascending index order:
- * out_idx[i] = j (int32), out_val[i] = grad[j] (bit copy), for the first
+ * out_idx[i] = j (int32, the state's own index), out_val[i] = grad[j] (bit copy), for the first
  * min(m, capacity) of them; *d_count (device int64) receives m, the number
  * transmitted, even when m > capacity.  capacity >= P never truncates.
  *   grad       device fp32 [P], this client's gradient

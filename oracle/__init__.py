@@ -41,7 +41,7 @@ def _load():
     lib.oracle_bfasgd_transmit.restype = ctypes.c_int
     lib.oracle_bfasgd_decide.argtypes = [i64, i64p, fp, f, f, u64, i64, i32, u8p]
     lib.oracle_bfasgd_decide.restype = None
-    lib.oracle_bfasgd_select.argtypes = [i64, fp, fp, f, f, u64, i64, i32, i32p, fp, i64]
+    lib.oracle_bfasgd_select.argtypes = [i64, fp, fp, f, f, u64, i64, i32, i32p, fp, i64, i64]
     lib.oracle_bfasgd_select.restype = ctypes.c_int64
     lib.oracle_bfasgd_apply_sparse.argtypes = [dp, dp, dp, dp, i64p, i64p, i32p, fp, i64, i64, d, d, d, d, i32]
     lib.oracle_bfasgd_apply_sparse.restype = ctypes.c_int
@@ -174,8 +174,10 @@ def bfasgd_decide(js, v_at, c, eps_c, seed, T, client) -> np.ndarray:
     return out.astype(bool)
 
 
-def bfasgd_select(v, grad, c, eps_c, seed, T, client, capacity=None):
-    """(idx int32 ascending, val fp32, count) for one client's push."""
+def bfasgd_select(v, grad, c, eps_c, seed, T, client, capacity=None, index_base=0):
+    """(idx int32 ascending, val fp32, count) for one client's push.  v and
+    grad may be the slice of a larger vector that starts at global index
+    index_base: decisions use the global index, the list the slice's own."""
     lib = _load()
     v = np.ascontiguousarray(v, dtype=np.float32)
     grad = np.ascontiguousarray(grad, dtype=np.float32)
@@ -187,7 +189,7 @@ def bfasgd_select(v, grad, c, eps_c, seed, T, client, capacity=None):
     val = np.zeros(max(cap, 1), dtype=np.float32)
     m = lib.oracle_bfasgd_select(P, _ptr(v, ctypes.c_float), _ptr(grad, ctypes.c_float), f32(c), f32(eps_c),
                                  int(seed) & (2**64 - 1), int(T), int(client),
-                                 _ptr(idx, ctypes.c_int32), _ptr(val, ctypes.c_float), cap)
+                                 _ptr(idx, ctypes.c_int32), _ptr(val, ctypes.c_float), cap, int(index_base))
     k = min(m, cap)
     return idx[:k].copy(), val[:k].copy(), int(m)
 

@@ -177,15 +177,18 @@ void oracle_bfasgd_decide(int64_t ns, const int64_t *js, const float *v_at, floa
 /*
  * Select and compact one client's gradient: every transmitted index in
  * ascending order with its gradient value.  Writes at most `capacity` entries
- * and returns the number transmitted (which may exceed capacity).
+ * and returns the number transmitted (which may exceed capacity).  The arrays
+ * may be a slice of a larger parameter vector that starts at global index
+ * index_base: decisions are keyed by the global index index_base + j, while
+ * the listed indices are the slice's own j.
  */
 int64_t oracle_bfasgd_select(int64_t P, const float *v, const float *grad, float c,
                              float eps_c, uint64_t seed, int64_t T, int32_t client,
-                             int32_t *idx, float *val, int64_t capacity)
+                             int32_t *idx, float *val, int64_t capacity, int64_t index_base)
 {
     int64_t m = 0;
     for (int64_t j = 0; j < P; ++j) {
-        if (oracle_bfasgd_transmit(j, v[j], c, eps_c, seed, T, client)) {
+        if (oracle_bfasgd_transmit(index_base + j, v[j], c, eps_c, seed, T, client)) {
             if (m < capacity) {
                 idx[m] = (int32_t)j;
                 val[m] = grad[j];

@@ -51,7 +51,7 @@ class fasgd_state(ctypes.Structure):
                 ("eps", ctypes.c_float), ("math_mode", ctypes.c_int32), ("v_reading", ctypes.c_int32),
                 ("T", ctypes.c_int64), ("dense_T", ctypes.c_int64),
                 ("theta", ctypes.c_void_p), ("n", ctypes.c_void_p), ("b", ctypes.c_void_p),
-                ("v", ctypes.c_void_p), ("last_T", ctypes.c_void_p)]
+                ("v", ctypes.c_void_p), ("last_T", ctypes.c_void_p), ("index_base", ctypes.c_int64)]
 
 
 _lib = None

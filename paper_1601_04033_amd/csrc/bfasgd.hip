@@ -6,8 +6,8 @@
 // never waits on another wave, so no launch has a block barrier in its
 // streaming part.  Selection runs in three or four launches:
 //   mark     the wave loads its tile of v, draws one Philox4x32-10 call per
-//            chunk (the counter is the chunk index j/4, so one call feeds one
-//            vector of v), forms four ballots per segment (1 bit per
+//            chunk (the counter is the global chunk index, so one call feeds
+//            one vector of v), forms four ballots per segment (1 bit per
 //            parameter), stores the tile's ballot words in one store and its
 //            transmit count;
 //   scan     one block per 1024 tiles scans their counts (offsets within the
@@ -94,8 +94,9 @@ __device__ __forceinline__ void mark_tile(const SelectArgs& a, int64_t tile, int
         const int64_t q = q0 + s * kWave;
         uint32_t nib = 0;
         if (FULL || q < nch) {
+            const uint64_t qg = a.chunk_base + static_cast<uint64_t>(q);   // global chunk index
             const uint4 w = philox4x32_10(
-                make_uint4(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), a.ctr_T, a.ctr_client),
+                make_uint4(static_cast<uint32_t>(qg), static_cast<uint32_t>(qg >> 32), a.ctr_T, a.ctr_client),
                 a.key0, a.key1);
             nib = transmit_bit(w.x, v[s][0], a.c, a.eps_c) | (transmit_bit(w.y, v[s][1], a.c, a.eps_c) << 1) |
                   (transmit_bit(w.z, v[s][2], a.c, a.eps_c) << 2) |

@@ -252,6 +252,9 @@ fasgd_status bfasgd_select_compact(const fasgd_state* st, const float* grad, flo
         (out_val && !aligned(out_val, 4)) || !aligned(d_count, 8))
         return fail(FASGD_ERR_ALIGN, "misaligned v, grad, output list or d_count");
     if (!aligned(workspace, 256)) return fail(FASGD_ERR_ALIGN, "workspace must be 256-byte aligned");
+    if (st->index_base < 0 || (st->index_base & 3) != 0 || st->index_base > (int64_t(1) << 62) - st->P)
+        return fail(FASGD_ERR_ARG, "index_base = %lld must be a multiple of 4 in [0, 2^62 - P]",
+                    (long long)st->index_base);
     if (workspace_bytes < fasgd::select_workspace_bytes(st->P))
         return fail(FASGD_ERR_CAPACITY, "workspace of %zu bytes is smaller than the %zu needed", workspace_bytes,
                     fasgd::select_workspace_bytes(st->P));
@@ -270,6 +273,7 @@ fasgd_status bfasgd_select_compact(const fasgd_state* st, const float* grad, flo
     a.key1 = static_cast<uint32_t>(seed >> 32);
     a.ctr_T = static_cast<uint32_t>(T);
     a.ctr_client = static_cast<uint32_t>(client);
+    a.chunk_base = static_cast<uint64_t>(st->index_base) >> 2;
     fasgd::select_workspace_layout(workspace, st->P, a);
     const bool vec = aligned(st->v, 16) && aligned(grad, 16);
     const hipError_t e = fasgd::launch_select(a, vec, stream);
@@ -424,6 +428,9 @@ fasgd_status bfasgd_decide_segments(const fasgd_state* st, const int64_t* seg, i
         return fail(FASGD_ERR_CLIENT, "client = %d is outside [0, %d)", client, st->lambda);
     if (!aligned(st->v, 4)) return fail(FASGD_ERR_ALIGN, "v is not 4-byte aligned");
     if (!aligned(workspace, 256)) return fail(FASGD_ERR_ALIGN, "workspace must be 256-byte aligned");
+    if (st->index_base < 0 || (st->index_base & 3) != 0 || st->index_base > (int64_t(1) << 62) - st->P)
+        return fail(FASGD_ERR_ARG, "index_base = %lld must be a multiple of 4 in [0, 2^62 - P]",
+                    (long long)st->index_base);
     if (workspace_bytes < fasgd::segments_workspace_bytes(st->P, S))
         return fail(FASGD_ERR_CAPACITY, "workspace of %zu bytes is smaller than the %zu needed", workspace_bytes,
                     fasgd::segments_workspace_bytes(st->P, S));

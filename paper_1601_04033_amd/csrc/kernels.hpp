@@ -56,6 +56,7 @@ struct SelectArgs {
     uint32_t key0, key1;    // seed low / high words
     uint32_t ctr_T;         // counter word 2
     uint32_t ctr_client;    // counter word 3
+    uint64_t chunk_base;    // global chunk index of chunk 0 (index_base / 4)
 };
 
 size_t select_workspace_bytes(int64_t P);

@@ -193,6 +193,12 @@ def test_select_rejects_bad_arguments(lib):
     assert sel(grad=f.ptr(5, misalign=1)) == 5
     big, f2 = _state(P=2 ** 31)
     assert sel(s=big) == 2
+    # a slice's global offset: a multiple of 4, >= 0, index_base + P <= 2^62
+    for base in (-4, 2, 2 ** 62 - 12):
+        st.index_base = base
+        assert sel() == 2
+        assert b"index_base" in lib.fasgd_last_error()
+    st.index_base = 0
 
 
 def test_sparse_rejects_bad_arguments(lib):

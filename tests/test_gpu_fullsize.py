@@ -200,3 +200,58 @@ def test_select_at_group_scan_switch(P):
     np.testing.assert_array_equal(val[:m].cpu().numpy().view(np.uint32), r_val.view(np.uint32))
     del st, gd, idx, val, cnt, ws
     _free()
+
+
+def test_shard_count_invariance():
+    """The state split into index-range shards (views of the same arrays,
+    each with its global offset as index_base) gives, shard by shard, the
+    whole state's results bit for bit: a K = 8 FASGD pass (elementwise) and
+    the B-FASGD selection (keyed by the global index), whose shard lists,
+    offset by each shard's base, concatenate to the whole list."""
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["tiny"]
+    P, K = 1_000_003, 8
+    theta0, m, s = workload.host_params(w, P, seed=3)
+    clients, ts = workload.schedule(w, K)
+    gs = [torch.from_numpy(workload.host_gradient(w, m, s, k, seed=3)).to(dev) for k in range(K)]
+    whole = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, fa.MATH_FAST)
+    fa.fasgd_apply_updates(whole, gs, clients, ts)
+    cuts = [0, 4, 262_144, 500_004, P]                      # multiples of 4, ragged last shard
+    theta, n, b, v, last_T = fa.allocate_state(P, dev)
+    theta.copy_(torch.from_numpy(theta0))
+    shards = []
+    for a, z in zip(cuts[:-1], cuts[1:]):
+        sh = fa.fasgd_init_state(theta[a:z], n[a:z], b[a:z], v[a:z], last_T[a:z], lam=w.lam,
+                                 alpha=w.alpha_fasgd, math_mode=fa.MATH_FAST)
+        sh.c.index_base = a
+        fa.fasgd_apply_updates(sh, [g[a:z] for g in gs], clients, ts)
+        shards.append(sh)
+    torch.cuda.synchronize()
+    for name in ("theta", "n", "b", "v"):
+        assert torch.equal(whole.tensors[name], locals()[name]), name
+    # selection of the next push, whole vs shards
+    g = gs[0]
+    c = 4.0 * float(v.median())
+    ws = fa.allocate_workspace(P, dev)
+    idx = torch.empty(P, device=dev, dtype=torch.int32)
+    val = torch.empty(P, device=dev)
+    cnt = torch.zeros(1, device=dev, dtype=torch.int64)
+    fa.bfasgd_select_compact(whole, g, c, 1e-8, SEED, K, 1, idx, val, cnt, ws)
+    torch.cuda.synchronize()
+    mw = int(cnt.item())
+    assert 0 < mw < P
+    want_i, want_v = idx[:mw].long().cpu(), val[:mw].cpu()
+    got_i, got_v = [], []
+    for (a, z), sh in zip(zip(cuts[:-1], cuts[1:]), shards):
+        fa.bfasgd_select_compact(sh, g[a:z], c, 1e-8, SEED, K, 1, idx, val, cnt, ws)
+        torch.cuda.synchronize()
+        ms = int(cnt.item())
+        got_i.append(idx[:ms].long().cpu() + a)
+        got_v.append(val[:ms].cpu())
+    assert torch.equal(torch.cat(got_i), want_i)
+    assert torch.equal(torch.cat(got_v).view(torch.int32), want_v.view(torch.int32))
+    # and both agree with the oracle's selection on the whole vector
+    r_i, r_v, r_m = oracle.bfasgd_select(v.cpu().numpy(), g.cpu().numpy(), c, 1e-8, SEED, K, 1)
+    assert r_m == mw
+    np.testing.assert_array_equal(want_i.numpy(), r_i)

@@ -197,3 +197,27 @@ def test_sparse_apply_leaves_unlisted_parameters():
     # an empty push is still one server update
     oracle.bfasgd_apply_sparse(st, np.zeros(0, np.int32), np.zeros(0, np.float32), grad_ts=1)
     assert st.T == 3
+
+
+def test_slices_with_index_base_reproduce_the_whole_selection():
+    """A vector cut into slices at global offsets (multiples of 4), each
+    selected with its offset as index_base, lists exactly the whole vector's
+    transmitted indices (slice index + offset) and values: decisions follow
+    the global index, so they do not depend on how the vector is cut."""
+    P = 50_003
+    v = workload.synthetic_v(P, seed=21)
+    g = np.random.default_rng(22).standard_normal(P).astype(np.float32)
+    idx, val, m = oracle.bfasgd_select(v, g, 30.0, 1e-8, 0xABC, 12, 3)
+    for cuts in ([0, P], [0, 4, 16_384, 30_000, P], [0, 25_000, P]):
+        parts_i, parts_v, total = [], [], 0
+        for a, b in zip(cuts[:-1], cuts[1:]):
+            i_s, v_s, m_s = oracle.bfasgd_select(v[a:b], g[a:b], 30.0, 1e-8, 0xABC, 12, 3, index_base=a)
+            parts_i.append(i_s.astype(np.int64) + a)
+            parts_v.append(v_s)
+            total += m_s
+        assert total == m
+        np.testing.assert_array_equal(np.concatenate(parts_i), idx)
+        np.testing.assert_array_equal(np.concatenate(parts_v).view(np.uint32), val.view(np.uint32))
+    # an offset that is not the slice's true position changes the decisions
+    i_w, _, _ = oracle.bfasgd_select(v[4:], g[4:], 30.0, 1e-8, 0xABC, 12, 3, index_base=0)
+    assert not np.array_equal(i_w + 4, idx[idx >= 4])
