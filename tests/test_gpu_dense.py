@@ -225,3 +225,31 @@ def test_rejected_call_changes_nothing():
     torch.cuda.synchronize()
     assert st.T == 0 and st.dense_T == -1
     assert (st.theta.cpu() == 1.0).all() and (st.last_T.cpu() == -1).all()
+
+
+@pytest.mark.parametrize("reading", [fa.V_EQUATIONS, fa.V_PROSE])
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("gamma,beta", [(1.0, 0.9), (0.95, 0.0), (1.0, 0.0), (0.5, 0.5)])
+def test_degenerate_decays(gamma, beta, mode, reading):
+    """Decay settings at the ends of [0, 1]: gamma = 1 freezes n and b at
+    their initial 0 (so v follows 1/sqrt(eps) or sqrt(eps)), beta = 0 makes
+    v the current term alone.  Four K = 8 passes over a ragged P against 32
+    single oracle updates."""
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["tiny"]
+    P, K = 4099, 8
+    theta0, m, s = workload.host_params(w, P, seed=6)
+    clients, ts = workload.schedule(w, 4 * K)
+    st = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, mode, gamma=gamma, beta=beta, v_reading=reading)
+    ref = oracle.init_state(theta0, alpha=w.alpha_fasgd, gamma=gamma, beta=beta, v_reading=reading)
+    for p in range(4):
+        gs = [workload.host_gradient(w, m, s, p * K + k, seed=6) for k in range(K)]
+        sl = slice(p * K, (p + 1) * K)
+        fa.fasgd_apply_updates(st, [to_dev(g, dev) for g in gs], clients[sl], ts[sl])
+        for k, g in enumerate(gs):
+            oracle.fasgd_apply(ref, g, ts[p * K + k])
+    torch.cuda.synchronize()
+    assert_state_close(st, ref, RTOL_SEQ, what=f"gamma={gamma} beta={beta}")
+    if gamma == 1.0:
+        assert (st.n.cpu() == 0).all() and (st.b.cpu() == 0).all()
