@@ -176,6 +176,12 @@ size_t bfasgd_workspace_bytes(int64_t P);
  * min(m, capacity) of them; *d_count (device int64) receives m, the number
  * transmitted, even when m > capacity.  capacity >= P never truncates.
  *   grad       device fp32 [P], this client's gradient
+ *   out_seg_start  optional (NULL: not written) device uint32
+ *              [bfasgd_list_index_length(P)], the list's index: entry s is the
+ *              list position of the first transmitted index >= 256 s (counted
+ *              before the capacity cut), the last entry is m.  It lets a
+ *              consumer find the entries of any 256-parameter segment at once
+ *              (fasgd_apply_with_push).
  *   c, eps_c   finite, >= 0
  *   T          server timestamp this push is applied at, 0 <= T < 2^32
  *   client     in [0, lambda)
@@ -187,8 +193,12 @@ size_t bfasgd_workspace_bytes(int64_t P);
 fasgd_status bfasgd_select_compact(const fasgd_state* st, const float* grad, float c, float eps_c,
                                    uint64_t seed, int64_t T, int32_t client,
                                    int32_t* out_idx, float* out_val, int64_t capacity,
-                                   int64_t* d_count, void* workspace, size_t workspace_bytes,
-                                   hipStream_t stream);
+                                   int64_t* d_count, uint32_t* out_seg_start,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Entries of the list index bfasgd_select_compact writes for P parameters:
+ * ceil(P / 256) + 1 (0 for P < 1). */
+int64_t bfasgd_list_index_length(int64_t P);
 
 /*
  * Server side of a B-FASGD push: the FASGD update of fasgd_apply_updates,
@@ -206,6 +216,31 @@ fasgd_status bfasgd_select_compact(const fasgd_state* st, const float* grad, flo
 fasgd_status bfasgd_apply_sparse(fasgd_state* st, const int32_t* idx, const float* val,
                                  const int64_t* d_count, int64_t capacity, int32_t client,
                                  int64_t grad_ts, hipStream_t stream);
+
+/*
+ * One pass that applies a compacted B-FASGD push and then K client gradients
+ * (Sec. 2.2, 2.3): the push at timestamp T (staleness T - push_grad_ts) to
+ * its listed parameters, exactly as bfasgd_apply_sparse, then the K
+ * gradients at T + 1 ... T + K, exactly as fasgd_apply_updates; each
+ * parameter's state stays in registers across all K + 1 updates.  The
+ * result is bit-identical to those two calls in that order (the order in
+ * which the server lock serialises a push that arrived ahead of K dense
+ * gradients), but the state is read and written once.  T advances by
+ * K + 1; listed parameters get last_T = T; dense_T becomes T + K.
+ *   push_idx, push_val, push_count, capacity  the push list, as for
+ *                      bfasgd_apply_sparse (indices ascending and distinct,
+ *                      as bfasgd_select_compact writes them)
+ *   push_seg_start     its index, as bfasgd_select_compact's out_seg_start
+ *   push_client, push_grad_ts  as for bfasgd_apply_sparse
+ *   grads, clients, grad_ts, K as for fasgd_apply_updates (K >= 1)
+ * Errors: those of the two calls it stands for (FASGD_ERR_NULL also for a
+ * NULL push_count or push_seg_start).
+ */
+fasgd_status fasgd_apply_with_push(fasgd_state* st, const int32_t* push_idx, const float* push_val,
+                                   const int64_t* push_count, const uint32_t* push_seg_start,
+                                   int64_t capacity, int32_t push_client, int64_t push_grad_ts,
+                                   const float* const* grads, const int32_t* clients,
+                                   const int64_t* grad_ts, int32_t K, hipStream_t stream);
 
 /*
  * Synchronous SGD server (Sec. 3, the apply-update listing): with the

@@ -35,6 +35,7 @@ ABI_FUNCTIONS = ("fasgd_init_state", "fasgd_apply_updates", "sasgd_apply_updates
                  "bfasgd_workspace_bytes", "bfasgd_select_compact", "bfasgd_apply_sparse",
                  "sgd_sync_apply", "bfasgd_apply_cached", "bfasgd_apply_fetch",
                  "bfasgd_segments_workspace_bytes", "bfasgd_decide_segments", "bfasgd_apply_segments",
+                 "bfasgd_list_index_length", "fasgd_apply_with_push",
                  "fasgd_status_string", "fasgd_last_error")
 
 
@@ -73,7 +74,10 @@ def load_library(path: Optional[str] = None):
     lib.sasgd_apply_updates.argtypes = [S, P, P, P, i32, P]
     lib.bfasgd_workspace_bytes.argtypes = [i64]
     lib.bfasgd_workspace_bytes.restype = sz
-    lib.bfasgd_select_compact.argtypes = [S, P, f, f, u64, i64, i32, P, P, i64, P, P, sz, P]
+    lib.bfasgd_select_compact.argtypes = [S, P, f, f, u64, i64, i32, P, P, i64, P, P, P, sz, P]
+    lib.bfasgd_list_index_length.argtypes = [i64]
+    lib.bfasgd_list_index_length.restype = i64
+    lib.fasgd_apply_with_push.argtypes = [S, P, P, P, P, i64, i32, i64, P, P, P, i32, P]
     lib.bfasgd_apply_sparse.argtypes = [S, P, P, P, i64, i32, i64, P]
     lib.sgd_sync_apply.argtypes = [S, P, f, P]
     lib.bfasgd_apply_cached.argtypes = [S, P, P, P, i64, P, i32, i64, P]
@@ -85,7 +89,7 @@ def load_library(path: Optional[str] = None):
     for name in ("fasgd_init_state", "fasgd_apply_updates", "sasgd_apply_updates",
                  "bfasgd_select_compact", "bfasgd_apply_sparse", "sgd_sync_apply",
                  "bfasgd_apply_cached", "bfasgd_apply_fetch", "bfasgd_decide_segments",
-                 "bfasgd_apply_segments"):
+                 "bfasgd_apply_segments", "fasgd_apply_with_push"):
         getattr(lib, name).restype = ctypes.c_int
     lib.fasgd_status_string.argtypes = [ctypes.c_int]
     lib.fasgd_status_string.restype = ctypes.c_char_p
@@ -211,11 +215,17 @@ def bfasgd_workspace_bytes(P: int) -> int:
     return int(load_library().bfasgd_workspace_bytes(int(P)))
 
 
+def bfasgd_list_index_length(P: int) -> int:
+    return int(load_library().bfasgd_list_index_length(int(P)))
+
+
 def bfasgd_select_compact(state: State, grad, c: float, eps_c: float, seed: int, T: int, client: int,
-                          out_idx, out_val, d_count, workspace, stream=None) -> None:
+                          out_idx, out_val, d_count, workspace, seg_start=None, stream=None) -> None:
     """Per-parameter send/skip selection of one client gradient, compacted
     into out_idx (int32) / out_val (fp32) in ascending index order; the
-    number transmitted goes to d_count (int64 [1], device)."""
+    number transmitted goes to d_count (int64 [1], device).  seg_start
+    (optional, int32 [bfasgd_list_index_length(P)], values < 2^31) receives
+    the list's index: the position of each 256-parameter segment's first entry."""
     import torch
     cap = out_idx.numel()
     if out_val.numel() != cap:
@@ -226,8 +236,35 @@ def bfasgd_select_compact(state: State, grad, c: float, eps_c: float, seed: int,
         ctypes.byref(state.c), _dev_ptr(grad, torch.float32, "grad"), c, eps_c,
         int(seed) & (2 ** 64 - 1), int(T), int(client),
         _dev_ptr(out_idx, torch.int32, "out_idx"), _dev_ptr(out_val, torch.float32, "out_val"), cap,
-        _dev_ptr(d_count, torch.int64, "d_count"), _dev_ptr(workspace, torch.uint8, "workspace"),
-        workspace.numel(), _stream(stream))
+        _dev_ptr(d_count, torch.int64, "d_count"), _seg_start_ptr(seg_start, state.P),
+        _dev_ptr(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
+    _check(rc)
+
+
+def _seg_start_ptr(seg_start, P, required=False):
+    import torch
+    if seg_start is None and not required:
+        return None
+    if seg_start is None or seg_start.numel() < bfasgd_list_index_length(P):
+        raise ValueError(f"seg_start needs bfasgd_list_index_length(P) = {bfasgd_list_index_length(P)} entries")
+    return _dev_ptr(seg_start, torch.int32, "seg_start")
+
+
+def fasgd_apply_with_push(state: State, push_idx, push_val, push_count, push_seg_start, push_client: int,
+                          push_grad_ts: int, grads: Sequence, clients: Sequence[int], grad_ts: Sequence[int],
+                          stream=None) -> None:
+    """One pass: the compacted push (at T, as bfasgd_apply_sparse) and then the K
+    gradients (at T + 1 ... T + K, as fasgd_apply_updates).  T advances by K + 1."""
+    import torch
+    cap = push_idx.numel()
+    if push_val.numel() != cap:
+        raise ValueError("push_idx and push_val must have the same capacity")
+    ptrs, c, t, K = _dense_args(state, grads, clients, grad_ts)
+    rc = load_library().fasgd_apply_with_push(
+        ctypes.byref(state.c), _dev_ptr(push_idx, torch.int32, "push_idx"),
+        _dev_ptr(push_val, torch.float32, "push_val"), _dev_ptr(push_count, torch.int64, "push_count"),
+        _seg_start_ptr(push_seg_start, state.P, required=True), cap, int(push_client), int(push_grad_ts),
+        ptrs, c, t, K, _stream(stream))
     _check(rc)
 
 

@@ -173,7 +173,10 @@ __device__ __forceinline__ void scan_groups(const SelectArgs& a, int64_t ng, boo
         carry += total;
         __syncthreads();
     }
-    if (threadIdx.x == 0) *a.d_count = static_cast<int64_t>(carry);
+    if (threadIdx.x == 0) {
+        *a.d_count = static_cast<int64_t>(carry);
+        if (a.seg_start) a.seg_start[a.n_segs] = carry;
+    }
 }
 
 // Group g of 1024 tiles: offsets of its tiles within the group and the group
@@ -261,6 +264,7 @@ __device__ __forceinline__ void scatter_tile(const SelectArgs& a, int64_t tile, 
     const uint64_t below = lanes_below(lane);
     int64_t base = static_cast<int64_t>(a.group_offset[tile / kScanBlock]) + a.tile_offset[tile];
     uint32_t staged = 0;
+    uint32_t seg_pos = 0;   // lane s < kTileSegs: list position of segment s's first entry
 #pragma unroll
     for (int s = 0; s < kTileSegs; ++s) {
         const uint64_t b0 = tb[4 * s], b1 = tb[4 * s + 1], b2 = tb[4 * s + 2], b3 = tb[4 * s + 3];
@@ -268,6 +272,7 @@ __device__ __forceinline__ void scatter_tile(const SelectArgs& a, int64_t tile, 
                              static_cast<uint32_t>(((b2 >> lane) & 1) << 2) |
                              static_cast<uint32_t>(((b3 >> lane) & 1) << 3);
         const uint32_t n_seg = __popcll(b0) + __popcll(b1) + __popcll(b2) + __popcll(b3);
+        if (lane == s) seg_pos = static_cast<uint32_t>(base + staged);
         if (staged + n_seg > static_cast<uint32_t>(kStageEntries)) {
             wave_lds_order();
             drain(a, s_idx, s_val, staged, base, lane);
@@ -291,6 +296,11 @@ __device__ __forceinline__ void scatter_tile(const SelectArgs& a, int64_t tile, 
     }
     wave_lds_order();
     drain(a, s_idx, s_val, staged, base, lane);
+    if (a.seg_start) {
+        static_assert(kTileSegs * kWave * 4 == kTileSegs * kPushSeg, "a tile segment is a list-index segment");
+        const int64_t sg = tile * kTileSegs + lane;
+        if (lane < kTileSegs && sg < a.n_segs) a.seg_start[sg] = seg_pos;
+    }
 }
 
 __global__ __launch_bounds__(kSelBlock) void select_scatter(const SelectArgs a, bool aligned)

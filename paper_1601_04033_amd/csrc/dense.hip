@@ -99,6 +99,144 @@ __global__ __launch_bounds__(kBlock) void fasgd_dense_vec(const DenseArgs a)
     }
 }
 
+// A compacted push applied in the same pass, before the K gradients (the
+// arrival order when the push came in ahead of them).  Every wave of the
+// vector kernel owns one kPushSeg-parameter segment (64 chunks of 4), so it
+// finds the push's entries for its parameters at [seg_start[s],
+// seg_start[s + 1]) of the list, clipped to min(count, capacity), and stages
+// them in its LDS slice: one value and one flag byte per parameter.
+constexpr int kWave = 64;
+constexpr int kWavesPerBlock = kBlock / kWave;
+static_assert(kWave * 4 == kPushSeg, "one vector-kernel wave covers one list-index segment");
+
+__device__ __forceinline__ void wave_lds_order()
+{
+    // the wave's LDS operations execute in order; keep the compiler from
+    // moving the reads of other lanes' entries above the writes
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Entries of segment seg, clipped to the list's usable length.
+__device__ __forceinline__ void push_range(const PushArgs& p, int64_t seg, int64_t& lo, int64_t& hi)
+{
+    int64_t m = *p.d_count;
+    m = m < p.capacity ? m : p.capacity;
+    m = m > 0 ? m : 0;
+    lo = hi = m;
+    if (seg < p.n_segs) {
+        const int64_t a0 = p.seg_start[seg], a1 = p.seg_start[seg + 1];
+        lo = a0 < m ? a0 : m;
+        hi = a1 < m ? a1 : m;
+    }
+}
+
+// Stage the entries of [lo, hi) whose index lies in [first, first + span)
+// (and below P): value at s_val[j - first], flag byte s_flag[j - first] = 1.
+// The flags must have been cleared.
+__device__ __forceinline__ void stage_push(const PushArgs& p, int64_t lo, int64_t hi, int64_t first, int span,
+                                           int64_t P, float* s_val, uint8_t* s_flag, int lane)
+{
+    for (int64_t e = lo + lane; e < hi; e += kWave) {
+        const int64_t x = static_cast<int64_t>(p.idx[e]) - first;
+        if (x >= 0 && x < span && first + x < P) {
+            s_val[x] = p.val[e];
+            s_flag[x] = 1;
+        }
+    }
+}
+
+template <int MODE>
+__global__ __launch_bounds__(kBlock) void fasgd_dense_push_vec(const DenseArgs a, const PushArgs p)
+{
+    __shared__ float s_val[kWavesPerBlock][kPushSeg];
+    __shared__ uint32_t s_flag[kWavesPerBlock][kWave];    // byte c of word l: parameter 4 l + c listed
+    const Hyper h = a.h;
+    const int K = a.K;
+    const int64_t nvec = a.P >> 2;
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int64_t seg = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + w;
+    const int64_t o = i * 4;
+    f4 th, n, b, v;
+    if (i < nvec) { th = ld4(a.theta + o); n = ld4(a.n + o); b = ld4(a.b + o); v = ld4(a.v + o); }
+    int64_t lo, hi;
+    push_range(p, seg, lo, hi);
+    s_flag[w][lane] = 0u;
+    wave_lds_order();
+    stage_push(p, lo, hi, seg * kPushSeg, kPushSeg, a.P, s_val[w], reinterpret_cast<uint8_t*>(s_flag[w]), lane);
+    wave_lds_order();
+    const uint32_t flags = s_flag[w][lane];
+    const f4 pv = *reinterpret_cast<const f4*>(&s_val[w][4 * lane]);
+    if (i < nvec) {
+        if (flags) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                if ((flags >> (8 * c)) & 0xffu) {
+                    float t = th[c], nn = n[c], bb = b[c], vv = v[c];
+                    fasgd_step<MODE>(t, nn, bb, vv, pv[c], p.coef, h);
+                    th[c] = t; n[c] = nn; b[c] = bb; v[c] = vv;
+                    p.last_T[o + c] = p.last_T_value;
+                }
+            }
+        }
+        int k = 0;
+        for (; k + kBatch <= K; k += kBatch) {
+            f4 g[kBatch];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) g[u] = ld4(a.grad[k + u] + o);
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) fasgd_step4<MODE>(th, n, b, v, g[u], a.coef[k + u], h);
+        }
+        for (; k < K; ++k) fasgd_step4<MODE>(th, n, b, v, ld4(a.grad[k] + o), a.coef[k], h);
+        st4(a.theta + o, th);
+        st4(a.n + o, n);
+        st4(a.b + o, b);
+        st4(a.v + o, v);
+    } else if (i == nvec) {
+        for (int64_t j = nvec * 4; j < a.P; ++j) {
+            const int c = static_cast<int>(j - nvec * 4);
+            float tt = a.theta[j], nn = a.n[j], bb = a.b[j], vv = a.v[j];
+            if ((flags >> (8 * c)) & 0xffu) {
+                fasgd_step<MODE>(tt, nn, bb, vv, pv[c], p.coef, h);
+                p.last_T[j] = p.last_T_value;
+            }
+            for (int k = 0; k < K; ++k) fasgd_step<MODE>(tt, nn, bb, vv, a.grad[k][j], a.coef[k], h);
+            a.theta[j] = tt; a.n[j] = nn; a.b[j] = bb; a.v[j] = vv;
+        }
+    }
+}
+
+// The same, one parameter per thread (arrays only 4-byte aligned): a wave
+// covers 64 parameters, a quarter of a list-index segment.
+template <int MODE>
+__global__ __launch_bounds__(kBlock) void fasgd_dense_push_scalar(const DenseArgs a, const PushArgs p)
+{
+    __shared__ float s_val[kWavesPerBlock][kWave];
+    __shared__ uint8_t s_flag[kWavesPerBlock][kWave];
+    const Hyper h = a.h;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int64_t first = static_cast<int64_t>(blockIdx.x) * kBlock + w * kWave;   // the wave's first parameter
+    const int64_t j = first + lane;
+    int64_t lo, hi;
+    push_range(p, first / kPushSeg, lo, hi);
+    s_flag[w][lane] = 0;
+    wave_lds_order();
+    stage_push(p, lo, hi, first, kWave, a.P, s_val[w], s_flag[w], lane);
+    wave_lds_order();
+    if (j >= a.P) return;
+    float th = a.theta[j], n = a.n[j], b = a.b[j], v = a.v[j];
+    if (s_flag[w][lane]) {
+        fasgd_step<MODE>(th, n, b, v, s_val[w][lane], p.coef, h);
+        p.last_T[j] = p.last_T_value;
+    }
+    for (int k = 0; k < a.K; ++k) fasgd_step<MODE>(th, n, b, v, a.grad[k][j], a.coef[k], h);
+    a.theta[j] = th; a.n[j] = n; a.b[j] = b; a.v[j] = v;
+}
+
 // Same update, one parameter per thread, for arrays that are only 4-byte aligned.
 template <int MODE>
 __global__ __launch_bounds__(kBlock) void fasgd_dense_scalar(const DenseArgs a)
@@ -221,6 +359,29 @@ void launch_dense_variant(const DenseArgs& a, bool aligned, unsigned grid, hipSt
         fasgd_dense_vec<VARIANT><<<grid, kBlock, 0, s>>>(a);
     else
         fasgd_dense_scalar<VARIANT><<<grid, kBlock, 0, s>>>(a);
+}
+
+template <int VARIANT>
+void launch_push_variant(const DenseArgs& a, const PushArgs& p, bool aligned, unsigned grid, hipStream_t s)
+{
+    if (aligned)
+        fasgd_dense_push_vec<VARIANT><<<grid, kBlock, 0, s>>>(a, p);
+    else
+        fasgd_dense_push_scalar<VARIANT><<<grid, kBlock, 0, s>>>(a, p);
+}
+
+hipError_t launch_fasgd_dense_push(const DenseArgs& a, const PushArgs& p, int variant, bool aligned,
+                                   hipStream_t s)
+{
+    const unsigned grid = aligned ? grid_for((a.P >> 2) + 1) : grid_for(a.P);
+    switch (variant) {
+    case kernel_variant(MATH_FAST, 0): launch_push_variant<kernel_variant(MATH_FAST, 0)>(a, p, aligned, grid, s); break;
+    case kernel_variant(MATH_IEEE, 0): launch_push_variant<kernel_variant(MATH_IEEE, 0)>(a, p, aligned, grid, s); break;
+    case kernel_variant(MATH_FAST, 1): launch_push_variant<kernel_variant(MATH_FAST, 1)>(a, p, aligned, grid, s); break;
+    case kernel_variant(MATH_IEEE, 1): launch_push_variant<kernel_variant(MATH_IEEE, 1)>(a, p, aligned, grid, s); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_fasgd_dense(const DenseArgs& a, int variant, bool aligned, hipStream_t s)

@@ -234,9 +234,16 @@ size_t bfasgd_workspace_bytes(int64_t P)
     return fasgd::select_workspace_bytes(P);
 }
 
+int64_t bfasgd_list_index_length(int64_t P)
+{
+    if (P < 1) return 0;
+    return fasgd::push_segments(P) + 1;
+}
+
 fasgd_status bfasgd_select_compact(const fasgd_state* st, const float* grad, float c, float eps_c, uint64_t seed,
                                    int64_t T, int32_t client, int32_t* out_idx, float* out_val, int64_t capacity,
-                                   int64_t* d_count, void* workspace, size_t workspace_bytes, hipStream_t stream)
+                                   int64_t* d_count, uint32_t* out_seg_start, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream)
 {
     if (!st) return fail(FASGD_ERR_NULL, "state is NULL");
     if (st->P < 1 || st->P > INT32_MAX) return fail(FASGD_ERR_ARG, "P must be in [1, INT32_MAX] for int32 indices");
@@ -249,8 +256,8 @@ fasgd_status bfasgd_select_compact(const fasgd_state* st, const float* grad, flo
     if (client < 0 || client >= st->lambda)
         return fail(FASGD_ERR_CLIENT, "client = %d is outside [0, %d)", client, st->lambda);
     if (!aligned(st->v, 4) || !aligned(grad, 4) || (out_idx && !aligned(out_idx, 4)) ||
-        (out_val && !aligned(out_val, 4)) || !aligned(d_count, 8))
-        return fail(FASGD_ERR_ALIGN, "misaligned v, grad, output list or d_count");
+        (out_val && !aligned(out_val, 4)) || !aligned(d_count, 8) || (out_seg_start && !aligned(out_seg_start, 4)))
+        return fail(FASGD_ERR_ALIGN, "misaligned v, grad, output list, d_count or out_seg_start");
     if (!aligned(workspace, 256)) return fail(FASGD_ERR_ALIGN, "workspace must be 256-byte aligned");
     if (st->index_base < 0 || (st->index_base & 3) != 0 || st->index_base > (int64_t(1) << 62) - st->P)
         return fail(FASGD_ERR_ARG, "index_base = %lld must be a multiple of 4 in [0, 2^62 - P]",
@@ -274,6 +281,8 @@ fasgd_status bfasgd_select_compact(const fasgd_state* st, const float* grad, flo
     a.ctr_T = static_cast<uint32_t>(T);
     a.ctr_client = static_cast<uint32_t>(client);
     a.chunk_base = static_cast<uint64_t>(st->index_base) >> 2;
+    a.seg_start = out_seg_start;
+    a.n_segs = fasgd::push_segments(st->P);
     fasgd::select_workspace_layout(workspace, st->P, a);
     const bool vec = aligned(st->v, 16) && aligned(grad, 16);
     const hipError_t e = fasgd::launch_select(a, vec, stream);
@@ -314,6 +323,47 @@ fasgd_status bfasgd_apply_sparse(fasgd_state* st, const int32_t* idx, const floa
         if (e != hipSuccess) return hip_fail(e, "bfasgd_apply_sparse");
     }
     st->T += 1;
+    return ok();
+}
+
+fasgd_status fasgd_apply_with_push(fasgd_state* st, const int32_t* push_idx, const float* push_val,
+                                   const int64_t* push_count, const uint32_t* push_seg_start, int64_t capacity,
+                                   int32_t push_client, int64_t push_grad_ts, const float* const* grads,
+                                   const int32_t* clients, const int64_t* grad_ts, int32_t K, hipStream_t stream)
+{
+    fasgd_status s = check_state(st, true);
+    if (s != FASGD_OK) return s;
+    if (!push_count || !push_seg_start) return fail(FASGD_ERR_NULL, "push_count or push_seg_start is NULL");
+    if (capacity < 0) return fail(FASGD_ERR_ARG, "capacity must be >= 0");
+    if (capacity > 0 && (!push_idx || !push_val)) return fail(FASGD_ERR_NULL, "push_idx or push_val is NULL");
+    if ((push_idx && !aligned(push_idx, 4)) || (push_val && !aligned(push_val, 4)) || !aligned(push_count, 8) ||
+        !aligned(push_seg_start, 4))
+        return fail(FASGD_ERR_ALIGN, "misaligned push_idx, push_val, push_count or push_seg_start");
+    float push_tau;
+    s = staleness(st, &push_client, &push_grad_ts, 1, &push_tau);
+    if (s != FASGD_OK) return s;
+    // the K gradients follow the push: they are applied at T + 1 ... T + K
+    fasgd_state after = *st;
+    after.T = st->T + 1;
+    fasgd::DenseArgs a;
+    bool vec = false;
+    s = dense_common(&after, grads, clients, grad_ts, K, true, a, vec);
+    if (s != FASGD_OK) return s;
+    fasgd::PushArgs p;
+    memset(&p, 0, sizeof p);
+    p.idx = push_idx;
+    p.val = push_val;
+    p.d_count = push_count;
+    p.seg_start = push_seg_start;
+    p.capacity = capacity;
+    p.n_segs = fasgd::push_segments(st->P);
+    p.last_T = st->last_T;
+    p.coef = st->math_mode == FASGD_MATH_FAST ? st->alpha / push_tau : push_tau;
+    p.last_T_value = static_cast<int32_t>(st->T);
+    const hipError_t e = fasgd::launch_fasgd_dense_push(a, p, variant_of(st), vec, stream);
+    if (e != hipSuccess) return hip_fail(e, "fasgd_apply_with_push");
+    st->dense_T = st->T + K;
+    st->T += K + 1;
     return ok();
 }
 

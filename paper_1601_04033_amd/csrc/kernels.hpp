@@ -57,6 +57,8 @@ struct SelectArgs {
     uint32_t ctr_T;         // counter word 2
     uint32_t ctr_client;    // counter word 3
     uint64_t chunk_base;    // global chunk index of chunk 0 (index_base / 4)
+    uint32_t* seg_start;    // optional: list position of each kPushSeg-parameter segment, [n_segs + 1]
+    int64_t n_segs;
 };
 
 size_t select_workspace_bytes(int64_t P);
@@ -81,6 +83,27 @@ struct SparseArgs {
 };
 
 hipError_t launch_sparse(const SparseArgs& a, int variant, hipStream_t s);
+
+// Index of a compacted list: seg_start[s] is the position of the first entry
+// with index >= kPushSeg * s, seg_start[n_segs] the number of entries.
+constexpr int kPushSeg = 256;
+inline int64_t push_segments(int64_t P) { return (P + kPushSeg - 1) / kPushSeg; }
+
+// A compacted push applied inside a dense pass, before its K gradients.
+struct PushArgs {
+    const int32_t* idx;
+    const float* val;
+    const int64_t* d_count;
+    const uint32_t* seg_start;
+    int64_t capacity;
+    int64_t n_segs;
+    int32_t* last_T;
+    float coef;             // as DenseArgs::coef for the push
+    int32_t last_T_value;   // the push's timestamp
+};
+
+hipError_t launch_fasgd_dense_push(const DenseArgs& a, const PushArgs& p, int variant, bool aligned,
+                                   hipStream_t s);
 
 // Paper-literal decisions per segment (groups of up to kSegGroup segments).
 constexpr int kSegGroup = 32;

@@ -177,9 +177,9 @@ def test_select_rejects_bad_arguments(lib):
     cnt = np.zeros(2, np.int64)
     cntp = (cnt.ctypes.data + 7) & ~7
 
-    def sel(c=1.0, eps_c=1e-8, T=0, client=0, cap=16, ws_ptr=wsp, ws_bytes=ws_need, grad=None, s=st):
+    def sel(c=1.0, eps_c=1e-8, T=0, client=0, cap=16, ws_ptr=wsp, ws_bytes=ws_need, grad=None, s=st, seg=None):
         return lib.bfasgd_select_compact(ctypes.byref(s), grad or f.ptr(5), c, eps_c, 7, T, client,
-                                         f.ptr(0), f.ptr(1), cap, cntp, ws_ptr, ws_bytes, None)
+                                         f.ptr(0), f.ptr(1), cap, cntp, seg, ws_ptr, ws_bytes, None)
 
     assert sel(c=-1.0) == 2
     assert sel(c=float("inf")) == 2
@@ -193,12 +193,39 @@ def test_select_rejects_bad_arguments(lib):
     assert sel(grad=f.ptr(5, misalign=1)) == 5
     big, f2 = _state(P=2 ** 31)
     assert sel(s=big) == 2
+    assert sel(seg=f.ptr(2, misalign=2)) == 5                        # the list index is uint32
     # a slice's global offset: a multiple of 4, >= 0, index_base + P <= 2^62
     for base in (-4, 2, 2 ** 62 - 12):
         st.index_base = base
         assert sel() == 2
         assert b"index_base" in lib.fasgd_last_error()
     st.index_base = 0
+
+
+def test_fused_push_rejects_bad_arguments(lib):
+    st, f = _state(P=16, T=2)
+    cnt = np.zeros(2, np.int64)
+    cntp = (cnt.ctypes.data + 7) & ~7
+
+    def fp(pc=0, pts=0, cap=16, count=cntp, seg="ok", ts=(0,), clients=None, K=None):
+        K = len(ts) if K is None else K
+        g = (ctypes.c_void_p * max(K, 1))(*([f.ptr(5)] * max(K, 1)))
+        c = (ctypes.c_int32 * max(K, 1))(*(clients or [0] * max(K, 1)))
+        t = (ctypes.c_int64 * max(K, 1))(*ts)
+        segp = f.ptr(3) if seg == "ok" else seg
+        return lib.fasgd_apply_with_push(ctypes.byref(st), f.ptr(0), f.ptr(1), count, segp, cap, pc, pts,
+                                         g, c, t, K, None)
+
+    assert fp(count=None) == 1
+    assert fp(seg=None) == 1
+    assert fp(seg=f.ptr(3, misalign=2)) == 5
+    assert fp(cap=-1) == 2
+    assert fp(pc=4) == 4                    # push client outside [0, lambda)
+    assert fp(pts=3) == 3                   # the push is applied at T = 2
+    assert fp(ts=(4,)) == 3                 # the first gradient is applied at T + 1 = 3
+    assert fp(ts=(0,), K=0) == 2
+    assert fp(ts=(0,), clients=[7]) == 4
+    assert st.T == 2 and st.dense_T == -1
 
 
 def test_sparse_rejects_bad_arguments(lib):

@@ -1,0 +1,152 @@
+"""GPU checks of a B-FASGD push applied inside the next dense pass
+(fasgd_apply_with_push): the list index that bfasgd_select_compact writes,
+bit-identity with the two separate calls it stands for (bfasgd_apply_sparse,
+then fasgd_apply_updates), and parity with the oracle applying the push and
+then the K gradients one by one."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1601_04033_amd as fa
+import workload
+from helpers import RTOL_SEQ, assert_state_close, gpu, new_gpu_state, to_dev
+
+pytestmark = pytest.mark.gpu
+SEED = 0x9E1EC7
+
+
+def _select(st, g, c, T, client, dev, cap=None):
+    import torch
+    P = st.P
+    cap = P if cap is None else cap
+    idx = torch.full((max(cap, 1),), -1, device=dev, dtype=torch.int32)[:cap]
+    val = torch.zeros(max(cap, 1), device=dev)[:cap]
+    cnt = torch.zeros(1, device=dev, dtype=torch.int64)
+    seg = torch.full((fa.bfasgd_list_index_length(P),), -1, device=dev, dtype=torch.int32)
+    fa.bfasgd_select_compact(st, g, c, 1e-8, SEED, T, client, idx, val, cnt, fa.allocate_workspace(P, dev),
+                             seg_start=seg)
+    return idx, val, cnt, seg
+
+
+def _states(P, dev, mode, reading, seed, offset=0):
+    """Two identical mid-run GPU states (the same synthetic n, b, v, theta,
+    T = 5) and the oracle state holding the same values; offset = 1 places the
+    arrays 4 bytes into their buffers (the scalar path)."""
+    import torch
+    w = workload.WORKLOADS["mlp_bfasgd"]
+    theta0, m_, s_ = workload.host_params(w, P, seed=seed)
+    b0 = m_ + s_ * np.float32(0.1)
+    n0 = (b0 * b0 + s_ * s_).astype(np.float32)
+    v0 = workload.synthetic_v(P, seed=seed, lo=5.0, hi=100.0)
+    out = []
+    for _ in range(2):
+        bufs = fa.allocate_state(P + offset, dev)
+        theta, n, b, v, last_T = (t[offset:] for t in bufs)
+        st = fa.fasgd_init_state(theta, n, b, v, last_T, lam=w.lam, alpha=w.alpha_fasgd, math_mode=mode,
+                                 v_reading=reading)
+        for t, a in ((theta, theta0), (n, n0), (b, b0), (v, v0)):
+            t.copy_(torch.from_numpy(a))
+        st.c.T = 5
+        out.append((st, bufs))
+    ref = oracle.init_state(theta0, alpha=w.alpha_fasgd, v_reading=reading)
+    ref.n, ref.b, ref.v = n0.astype(np.float64), b0.astype(np.float64), v0.astype(np.float64)
+    ref.T = 5
+    return out[0][0], out[1][0], ref, (m_, s_, w), (out[0][1], out[1][1])
+
+
+def _assert_same(a, b):
+    import torch
+    torch.cuda.synchronize()
+    for name in ("theta", "n", "b", "v", "last_T"):
+        assert torch.equal(a.tensors[name], b.tensors[name]), name
+    assert a.T == b.T and a.dense_T == b.dense_T
+
+
+@pytest.mark.parametrize("P", [1, 255, 257, 100_003, 1_000_003])
+def test_list_index_points_at_each_segment(P):
+    """seg_start[s] is the position of the first listed index >= 256 s and
+    the last entry is the count, at fractions from nothing to everything."""
+    import torch
+    dev = gpu()
+    v = workload.synthetic_v(P, seed=P % 97)
+    st = new_gpu_state(np.zeros(P, np.float32), dev, 16, 0.005, fa.MATH_FAST)
+    st.v.copy_(torch.from_numpy(v))
+    g = torch.randn(P, device=dev)
+    for c in (0.0, 40.0, 3e38):
+        idx, val, cnt, seg = _select(st, g, c, 11, 2, dev)
+        torch.cuda.synchronize()
+        m = int(cnt.item())
+        lst = idx[:m].cpu().numpy().astype(np.int64)
+        want = np.searchsorted(lst, 256 * np.arange(fa.bfasgd_list_index_length(P) - 1))
+        got = seg.cpu().numpy().astype(np.int64)
+        np.testing.assert_array_equal(got[:-1], want)
+        assert got[-1] == m
+
+
+@pytest.mark.parametrize("reading", [fa.V_EQUATIONS, fa.V_PROSE])
+@pytest.mark.parametrize("mode", [fa.MATH_FAST, fa.MATH_IEEE])
+@pytest.mark.parametrize("P,K,offset", [(100_003, 8, 0), (1_000_003, 33, 0), (65_537, 1, 1), (1027, 64, 0)])
+def test_push_inside_pass_is_bit_identical(P, K, offset, mode, reading):
+    """A push at about 30 % followed by K gradients: one fused pass gives the
+    state, last_T, T and dense_T of the two separate calls bit for bit
+    (vector path with a ragged tail, and the scalar path for arrays 4 bytes
+    off 16-byte alignment)."""
+    dev = gpu()
+    a, b, _, (m_, s_, w), keep = _states(P, dev, mode, reading, seed=P % 1000, offset=offset)
+    g_push = to_dev(workload.host_gradient(w, m_, s_, 5, seed=3), dev)
+    gs = [to_dev(workload.host_gradient(w, m_, s_, 6 + k, seed=3), dev) for k in range(K)]
+    clients, ts = list(range(K)), [max(6 + k - 3, 0) for k in range(K)]
+    idx, val, cnt, seg = _select(a, g_push, 100.0, 5, 1, dev)
+    fa.bfasgd_apply_sparse(a, idx, val, cnt, 1, 4)
+    fa.fasgd_apply_updates(a, gs, [c % w.lam for c in clients], ts)
+    fa.fasgd_apply_with_push(b, idx, val, cnt, seg, 1, 4, gs, [c % w.lam for c in clients], ts)
+    _assert_same(a, b)
+    assert b.T == 5 + K + 1 and b.dense_T == 5 + K
+
+
+@pytest.mark.parametrize("case", ["truncated", "empty", "all"])
+def test_push_inside_pass_edge_lists(case):
+    """A list cut by capacity, an empty push and a push of every parameter."""
+    import torch
+    dev = gpu()
+    P, K = 200_003, 4
+    a, b, _, (m_, s_, w), keep = _states(P, dev, fa.MATH_FAST, fa.V_EQUATIONS, seed=7)
+    g_push = to_dev(workload.host_gradient(w, m_, s_, 5, seed=7), dev)
+    gs = [to_dev(workload.host_gradient(w, m_, s_, 6 + k, seed=7), dev) for k in range(K)]
+    c = {"truncated": 100.0, "empty": 3e38, "all": 0.0}[case]
+    cap = 12_345 if case == "truncated" else None
+    idx, val, cnt, seg = _select(a, g_push, c, 5, 1, dev, cap=cap)
+    torch.cuda.synchronize()
+    m = int(cnt.item())
+    if case == "truncated":
+        assert m > 12_345
+    elif case == "all":
+        assert m == P
+    fa.bfasgd_apply_sparse(a, idx, val, cnt, 1, 5)
+    fa.fasgd_apply_updates(a, gs, [0, 1, 2, 3], [6, 5, 4, 3])
+    fa.fasgd_apply_with_push(b, idx, val, cnt, seg, 1, 5, gs, [0, 1, 2, 3], [6, 5, 4, 3])
+    _assert_same(a, b)
+
+
+def test_push_inside_pass_matches_oracle():
+    """Against the oracle: the same list applied as a sparse push at T = 5,
+    then 16 gradients one by one."""
+    import torch
+    dev = gpu()
+    P, K = 300_007, 16
+    _, st, ref, (m_, s_, w), keep = _states(P, dev, fa.MATH_FAST, fa.V_EQUATIONS, seed=12)
+    g_push = workload.host_gradient(w, m_, s_, 5, seed=12)
+    gs = [workload.host_gradient(w, m_, s_, 6 + k, seed=12) for k in range(K)]
+    ts = [max(6 + k - 5, 0) for k in range(K)]
+    clients = [k % w.lam for k in range(K)]
+    idx, val, cnt, seg = _select(st, to_dev(g_push, dev), 100.0, 5, 3, dev)
+    fa.fasgd_apply_with_push(st, idx, val, cnt, seg, 3, 2, [to_dev(g, dev) for g in gs], clients, ts)
+    r_idx, r_val, r_m = oracle.bfasgd_select(ref.v.astype(np.float32), g_push, 100.0, 1e-8, SEED, 5, 3)
+    oracle.bfasgd_apply_sparse(ref, r_idx, r_val, 2)
+    for g, t in zip(gs, ts):
+        oracle.fasgd_apply(ref, g, t)
+    torch.cuda.synchronize()
+    assert int(cnt.item()) == r_m
+    assert_state_close(st, ref, RTOL_SEQ, what="push then 16 gradients")
+    lt = st.last_T.cpu().numpy()
+    assert (lt[r_idx] == 5).all() and (np.delete(lt, r_idx) == -1).all()
