@@ -134,37 +134,54 @@ def main():
     val = torch.empty(cap, device=dev)
     cnt = torch.zeros(1, device=dev, dtype=torch.int64)
     ws = fa.allocate_workspace(P, dev)
+    seg = torch.empty(fa.bfasgd_list_index_length(P), device=dev, dtype=torch.int32)
     per_step = K + 1
-    # timestamps used: K (first pass) + (K + 1) per step, then the legs after
-    # the timed region: 3 SASGD passes of K, 3 cached pushes, 3 segment
-    # pushes and 3 synchronous steps
-    # and the dense passes at K = 1, 8, 32 (11 calls each)
+    # timestamps used: K (first pass) + (K + 1) per step + 1 (the last push),
+    # then the legs after the timed region: 3 steps of separate calls, 3
+    # SASGD passes of K, 3 cached pushes, 3 segment pushes, 3 synchronous
+    # steps and the dense passes at K = 1, 8, 32 (11 calls each)
     KS = (1, 8, 32)
-    clients, ts = workload.schedule(w, K + (warm + steps) * per_step + 3 * K + 9 + 16 + 11 * sum(KS))
+    clients, ts = workload.schedule(w, K + (warm + steps + 3) * per_step + 1 + 3 * K + 9 + 16 + 11 * sum(KS))
     torch.cuda.synchronize()
 
-    ev = {name: [] for name in ("dense", "select", "sparse")}
+    # One step: a single pass that applies the push selected in the previous
+    # step (at its timestamp T) and then K client gradients (T + 1 ... T + K),
+    # then the selection of this step's push (applied at T + K + 1 by the
+    # next pass).  That is the order in which the server lock serialises the
+    # arrivals, and per step the work is K dense updates, one push selected
+    # and one push applied.  The first step of the warm-up has no push to
+    # apply; the push selected by the last timed step is applied after the
+    # timed region.
+    ev = {name: [] for name in ("pass", "select")}
     counts = []
+    pending = []                              # (client, grad_ts) of the selected, unapplied push
 
     def step(timed, c):
         base = st.T                          # the schedule is indexed by server timestamp
-        sl = slice(base, base + K)
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e2 = torch.cuda.Event(enable_timing=True)
-        e3 = torch.cuda.Event(enable_timing=True)
         e0.record()
-        fa.fasgd_apply_updates(st, pool[:K], clients[sl], ts[sl])
+        applied = None
+        if pending:
+            pc, pts = pending.pop()
+            sl = slice(base + 1, base + 1 + K)
+            fa.fasgd_apply_with_push(st, idx, val, cnt, seg, pc, pts, pool[:K], clients[sl], ts[sl])
+            applied = cnt.clone()            # entries applied, read before the next selection
+        else:
+            sl = slice(base, base + K)
+            fa.fasgd_apply_updates(st, pool[:K], clients[sl], ts[sl])
         e1.record()
-        fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, st.T, clients[base + K], idx, val, cnt, ws)
+        T_sel = st.T
+        fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, T_sel, clients[T_sel], idx, val, cnt, ws,
+                                 seg_start=seg)
         e2.record()
-        fa.bfasgd_apply_sparse(st, idx, val, cnt, clients[base + K], ts[base + K])
-        e3.record()
+        pending.append((clients[T_sel], ts[T_sel]))
         if timed:
-            ev["dense"].append((e0, e1))
             ev["select"].append((e1, e2))
-            ev["sparse"].append((e2, e3))
-            counts.append(cnt.clone())
+            if applied is not None:
+                ev["pass"].append((e0, e1))
+                counts.append(applied)
 
     # the first dense pass gives v its scale; c is then fixed for the run
     fa.fasgd_apply_updates(st, pool[:K], clients[:K], ts[:K])
@@ -183,18 +200,42 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     print(f"# timed {steps} steps in {wall:.3f} s", file=sys.stderr, flush=True)
+    # the last push is applied after the timed region
+    pc, pts = pending.pop()
+    fa.bfasgd_apply_sparse(st, idx, val, cnt, pc, pts)
 
     ms = {k: [a.elapsed_time(b_) for a, b_ in pairs] for k, pairs in ev.items()}
     m_list = [int(x.item()) for x in counts]
-    m_avg = float(np.mean(m_list))
+    m_avg = float(np.mean(m_list)) if m_list else 0.0
     updates = steps * P * K + sum(m_list)
     value = updates / wall
-    dense_ms = float(np.mean(ms["dense"]))
-    dense_bytes = P * (32 + 4 * K)          # per launch: state 16 B read + 16 B write, 4 B per gradient
-    achieved = dense_bytes / (dense_ms * 1e-3) / 1e9
+    pass_ms = float(np.mean(ms["pass"])) if ms["pass"] else float("nan")
+    # per launch: state 16 B read + 16 B write, 4 B per gradient, and for the
+    # push 4 B index + 4 B value per entry and its list index
+    pass_bytes = P * (32 + 4 * K) + 8 * m_avg + 4 * fa.bfasgd_list_index_length(P)
+    achieved = pass_bytes / (pass_ms * 1e-3) / 1e9
     traffic = measured_traffic(P, K)
-    sel_ms, sp_ms = float(np.mean(ms["select"])), float(np.mean(ms["sparse"]))
+    sel_ms = float(np.mean(ms["select"]))
     sel_bytes = P * 8 + m_avg * 8                   # v + g read, (idx, val) written
+
+    # the same steps as three separate calls (dense pass, selection, sparse
+    # apply), for comparison
+    sep_ms, sp_ms = [], []
+    for r in range(3):
+        base = st.T
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e[0].record()
+        fa.fasgd_apply_updates(st, pool[:K], clients[base:base + K], ts[base:base + K])
+        e[1].record()
+        fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, st.T, clients[base + K], idx, val, cnt, ws)
+        e[2].record()
+        fa.bfasgd_apply_sparse(st, idx, val, cnt, clients[base + K], ts[base + K])
+        e[3].record()
+        torch.cuda.synchronize()
+        sep_ms.append(e[0].elapsed_time(e[3]))
+        sp_ms.append(e[2].elapsed_time(e[3]))
+    sep_ms_avg = float(np.mean(sep_ms[1:]))
+    sp_ms = float(np.mean(sp_ms[1:]))
     sp_bytes = m_avg * 44                           # idx, val + 16 B state gather, 16 B scatter, 4 B last_T
 
     # SASGD mode of the same pass, measured after the timed region
@@ -305,16 +346,21 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": f"{args.workload}: {w.name}, P={P}, lambda={w.lam}, K={K} fused FASGD "
-                               f"updates + 1 B-FASGD push at ~{int(f * 100)}% per step, {args.math} math",
+        "config": {"workload": f"{args.workload}: {w.name}, P={P}, lambda={w.lam}, per step one pass applying "
+                               f"the previous B-FASGD push (~{int(f * 100)}% transmitted) and K={K} FASGD "
+                               f"updates, then the next push's selection; {args.math} math",
                    "P": P, "K": K, "lambda": w.lam, "math": args.math, "transmit_fraction": f, "c": c},
-        "roofline": {"bound": "hbm", "kernel": "fasgd_dense_vec", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": traffic, "algorithmic_bytes": dense_bytes},
+        "roofline": {"bound": "hbm", "kernel": "fasgd_dense_push_vec", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic, "algorithmic_bytes": pass_bytes},
         "kernels": {
-            "fasgd_apply_updates": {"ms": dense_ms, "GB/s": achieved,
-                                    "param_updates_per_s": P * K / (dense_ms * 1e-3),
+            "fasgd_apply_with_push": {"ms": pass_ms, "GB/s": achieved,
+                                      "param_updates_per_s": (P * K + m_avg) / (pass_ms * 1e-3)},
+            "fasgd_apply_updates": {"ms": dense_k[str(K)]["ms"] if str(K) in dense_k else None,
+                                    "GB/s": dense_k[str(K)]["GB/s"] if str(K) in dense_k else None,
                                     "back_to_back_by_K": dense_k},
+            "step_as_separate_calls": {"ms": sep_ms_avg,
+                                       "calls": "fasgd_apply_updates, bfasgd_select_compact, bfasgd_apply_sparse"},
             "bfasgd_select_compact": {"ms": sel_ms, "GB/s": sel_bytes / (sel_ms * 1e-3) / 1e9,
                                       "ms_back_to_back": sel_b2b_ms,
                                       "GB/s_back_to_back": sel_b2b_bytes / (sel_b2b_ms * 1e-3) / 1e9,

@@ -77,7 +77,8 @@ typedef enum fasgd_v_reading {
  * Per-parameter staleness bookkeeping: a dense apply updates every
  * parameter, so it records its timestamp once in dense_T instead of
  * writing P copies of it; the last update that touched parameter j is
- * max(last_T[j], dense_T) (-1: never updated).
+ * max(last_T[j], dense_T) (-1: never updated).  A value of last_T[j] at or
+ * below dense_T carries no information.
  * index_base: a state may hold the slice [index_base, index_base + P) of a
  * larger parameter vector (one shard of a server split by index range).  The
  * updates are elementwise and ignore it; B-FASGD decisions draw their random
@@ -222,11 +223,14 @@ fasgd_status bfasgd_apply_sparse(fasgd_state* st, const int32_t* idx, const floa
  * (Sec. 2.2, 2.3): the push at timestamp T (staleness T - push_grad_ts) to
  * its listed parameters, exactly as bfasgd_apply_sparse, then the K
  * gradients at T + 1 ... T + K, exactly as fasgd_apply_updates; each
- * parameter's state stays in registers across all K + 1 updates.  The
- * result is bit-identical to those two calls in that order (the order in
- * which the server lock serialises a push that arrived ahead of K dense
+ * parameter's state stays in registers across all K + 1 updates.  theta,
+ * n, b and v are bit-identical to those two calls in that order (the order
+ * in which the server lock serialises a push that arrived ahead of K dense
  * gradients), but the state is read and written once.  T advances by
- * K + 1; listed parameters get last_T = T; dense_T becomes T + K.
+ * K + 1 and dense_T becomes T + K.  last_T is not written: every
+ * parameter's last update is the dense one at T + K, so the last update
+ * max(last_T[j], dense_T) of every parameter is the same as after the two
+ * calls, without the push's scattered timestamp writes.
  *   push_idx, push_val, push_count, capacity  the push list, as for
  *                      bfasgd_apply_sparse (indices ascending and distinct,
  *                      as bfasgd_select_compact writes them)

@@ -105,6 +105,11 @@ __global__ __launch_bounds__(kBlock) void fasgd_dense_vec(const DenseArgs a)
 // finds the push's entries for its parameters at [seg_start[s],
 // seg_start[s + 1]) of the list, clipped to min(count, capacity), and stages
 // them in its LDS slice: one value and one flag byte per parameter.
+// last_T is not written: the K gradients that follow update every parameter
+// later than the push, and that last update is recorded once as dense_T
+// (scattered 4-byte timestamp writes cost this pass about 8 % at 1e9
+// parameters and a 10 % push; without them the pass takes as long as the
+// dense pass alone).
 constexpr int kWave = 64;
 constexpr int kWavesPerBlock = kBlock / kWave;
 static_assert(kWave * 4 == kPushSeg, "one vector-kernel wave covers one list-index segment");
@@ -159,18 +164,43 @@ __global__ __launch_bounds__(kBlock) void fasgd_dense_push_vec(const DenseArgs a
     const int lane = threadIdx.x & (kWave - 1);
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int64_t seg = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + w;
+    const int64_t first = seg * kPushSeg;
     const int64_t o = i * 4;
-    f4 th, n, b, v;
-    if (i < nvec) { th = ld4(a.theta + o); n = ld4(a.n + o); b = ld4(a.b + o); v = ld4(a.v + o); }
+    // Loads in the order their data is needed, so that waiting for the list
+    // entries does not wait for the state and gradient loads behind them:
+    // the first 64 entries of the segment, then the state, then the first
+    // batch of gradients.
     int64_t lo, hi;
     push_range(p, seg, lo, hi);
+    int32_t e_idx = -1;
+    float e_val = 0.0f;
+    if (lo + lane < hi) { e_idx = p.idx[lo + lane]; e_val = p.val[lo + lane]; }
+    const bool own = i < nvec;
+    f4 th, n, b, v;
+    if (own) { th = ld4(a.theta + o); n = ld4(a.n + o); b = ld4(a.b + o); v = ld4(a.v + o); }
+    const int k0 = K < kBatch ? K : kBatch;
+    f4 g0[kBatch];
+    if (own) {
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u)
+            if (u < k0) g0[u] = ld4(a.grad[u] + o);
+    }
+    // stage the push's entries for this segment
     s_flag[w][lane] = 0u;
     wave_lds_order();
-    stage_push(p, lo, hi, seg * kPushSeg, kPushSeg, a.P, s_val[w], reinterpret_cast<uint8_t*>(s_flag[w]), lane);
+    {
+        const int64_t x = static_cast<int64_t>(e_idx) - first;
+        if (e_idx >= 0 && x >= 0 && x < kPushSeg && first + x < a.P) {
+            s_val[w][x] = e_val;
+            reinterpret_cast<uint8_t*>(s_flag[w])[x] = 1;
+        }
+    }
+    if (hi - lo > kWave)   // more than 64 entries in 256 parameters (transmit fraction above 1/4)
+        stage_push(p, lo + kWave, hi, first, kPushSeg, a.P, s_val[w], reinterpret_cast<uint8_t*>(s_flag[w]), lane);
     wave_lds_order();
     const uint32_t flags = s_flag[w][lane];
     const f4 pv = *reinterpret_cast<const f4*>(&s_val[w][4 * lane]);
-    if (i < nvec) {
+    if (own) {
         if (flags) {
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
@@ -178,11 +208,13 @@ __global__ __launch_bounds__(kBlock) void fasgd_dense_push_vec(const DenseArgs a
                     float t = th[c], nn = n[c], bb = b[c], vv = v[c];
                     fasgd_step<MODE>(t, nn, bb, vv, pv[c], p.coef, h);
                     th[c] = t; n[c] = nn; b[c] = bb; v[c] = vv;
-                    p.last_T[o + c] = p.last_T_value;
                 }
             }
         }
-        int k = 0;
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u)
+            if (u < k0) fasgd_step4<MODE>(th, n, b, v, g0[u], a.coef[u], h);
+        int k = k0;
         for (; k + kBatch <= K; k += kBatch) {
             f4 g[kBatch];
 #pragma unroll
@@ -199,10 +231,7 @@ __global__ __launch_bounds__(kBlock) void fasgd_dense_push_vec(const DenseArgs a
         for (int64_t j = nvec * 4; j < a.P; ++j) {
             const int c = static_cast<int>(j - nvec * 4);
             float tt = a.theta[j], nn = a.n[j], bb = a.b[j], vv = a.v[j];
-            if ((flags >> (8 * c)) & 0xffu) {
-                fasgd_step<MODE>(tt, nn, bb, vv, pv[c], p.coef, h);
-                p.last_T[j] = p.last_T_value;
-            }
+            if ((flags >> (8 * c)) & 0xffu) fasgd_step<MODE>(tt, nn, bb, vv, pv[c], p.coef, h);
             for (int k = 0; k < K; ++k) fasgd_step<MODE>(tt, nn, bb, vv, a.grad[k][j], a.coef[k], h);
             a.theta[j] = tt; a.n[j] = nn; a.b[j] = bb; a.v[j] = vv;
         }
@@ -229,10 +258,7 @@ __global__ __launch_bounds__(kBlock) void fasgd_dense_push_scalar(const DenseArg
     wave_lds_order();
     if (j >= a.P) return;
     float th = a.theta[j], n = a.n[j], b = a.b[j], v = a.v[j];
-    if (s_flag[w][lane]) {
-        fasgd_step<MODE>(th, n, b, v, s_val[w][lane], p.coef, h);
-        p.last_T[j] = p.last_T_value;
-    }
+    if (s_flag[w][lane]) fasgd_step<MODE>(th, n, b, v, s_val[w][lane], p.coef, h);
     for (int k = 0; k < a.K; ++k) fasgd_step<MODE>(th, n, b, v, a.grad[k][j], a.coef[k], h);
     a.theta[j] = th; a.n[j] = n; a.b[j] = b; a.v[j] = v;
 }

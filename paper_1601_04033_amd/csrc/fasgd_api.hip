@@ -357,9 +357,7 @@ fasgd_status fasgd_apply_with_push(fasgd_state* st, const int32_t* push_idx, con
     p.seg_start = push_seg_start;
     p.capacity = capacity;
     p.n_segs = fasgd::push_segments(st->P);
-    p.last_T = st->last_T;
     p.coef = st->math_mode == FASGD_MATH_FAST ? st->alpha / push_tau : push_tau;
-    p.last_T_value = static_cast<int32_t>(st->T);
     const hipError_t e = fasgd::launch_fasgd_dense_push(a, p, variant_of(st), vec, stream);
     if (e != hipSuccess) return hip_fail(e, "fasgd_apply_with_push");
     st->dense_T = st->T + K;

@@ -97,9 +97,7 @@ struct PushArgs {
     const uint32_t* seg_start;
     int64_t capacity;
     int64_t n_segs;
-    int32_t* last_T;
     float coef;             // as DenseArgs::coef for the push
-    int32_t last_T_value;   // the push's timestamp
 };
 
 hipError_t launch_fasgd_dense_push(const DenseArgs& a, const PushArgs& p, int variant, bool aligned,
