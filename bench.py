@@ -28,7 +28,7 @@ METRIC = "param-updates/sec and achieved HBM GB/s (% of peak), FASGD apply at 25
 HBM_PEAK_GBS = 8000.0
 EPS_C = 1e-8
 SEED = 0x5EED
-PMC_SUMMARY = os.path.join(ROOT, "profiles", "fasgd_dense_k32_memscale_1e9_pmc.txt")
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "fasgd_dense_push_k32_memscale_1e9_pmc.txt")
 DENSE_SOURCES = [os.path.join(ROOT, "paper_1601_04033_amd", "csrc", f) for f in ("dense.hip", "device_math.hpp")]
 
 
