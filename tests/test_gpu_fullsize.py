@@ -101,6 +101,76 @@ def test_memscale_1e9_step_sampled():
     _free()
 
 
+def test_memscale_1e9_fused_step_sampled():
+    """The benchmark's step at 1e9 parameters: a K = 32 pass, the push
+    selected at about 10 % with its list index, then one pass applying that
+    push and 32 more gradients (fasgd_apply_with_push), on 4096 sampled
+    parameters against the oracle (near-ties of the fp32 v drift excluded)."""
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["memscale"]
+    P, K = w.P, 32
+    free, total = torch.cuda.mem_get_info()
+    if free < 170e9:
+        pytest.skip(f"needs about 170 GB of free device memory, {free / 1e9:.0f} GB free")
+    print(f"memscale fused step: P={P} K={K}", flush=True)
+    theta0, m, s = workload.device_params(w, dev)
+    clients, ts = workload.schedule(w, 2 * K + 1)
+    js = sample_indices(P, 4096, seed=2)
+    jt = torch.from_numpy(js).to(dev)
+    st = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, fa.MATH_FAST)
+    ref = oracle.init_state(theta0[jt].cpu().numpy(), alpha=w.alpha_fasgd)
+    del theta0
+    grads = [workload.device_gradient(w, m, s, t) for t in range(K + 1)]
+    del m, s
+    g_host = [g[jt].cpu().numpy() for g in grads]
+    fa.fasgd_apply_updates(st, grads[:K], clients[:K], ts[:K])
+    for k in range(K):
+        oracle.fasgd_apply(ref, g_host[k], ts[k])
+    c = _calibrate_c(ref.v, w.transmit_fraction)
+    cap = P // 4
+    idx = torch.empty(cap, device=dev, dtype=torch.int32)
+    val = torch.empty(cap, device=dev)
+    cnt = torch.zeros(1, device=dev, dtype=torch.int64)
+    seg = torch.empty(fa.bfasgd_list_index_length(P), device=dev, dtype=torch.int32)
+    ws = fa.allocate_workspace(P, dev)
+    fa.bfasgd_select_compact(st, grads[K], c, 1e-8, SEED, st.T, clients[K], idx, val, cnt, ws, seg_start=seg)
+    torch.cuda.synchronize()
+    mm = int(cnt.item())
+    assert 0.08 < mm / P < 0.12, mm / P
+    # the index against the list, at sampled segments
+    segs = np.unique(js // 256)
+    starts = seg[torch.from_numpy(segs).to(dev)].long()
+    want_starts = torch.searchsorted(idx[:mm], torch.from_numpy(segs * 256).to(dev).to(torch.int32))
+    assert torch.equal(starts, want_starts)
+    assert int(seg[-1].item()) == mm
+    # which sampled parameters the push carries (both sides decide from the same-state v)
+    lst = idx[:mm]
+    pos = torch.searchsorted(lst, jt.to(torch.int32))
+    got = ((pos < mm) & (lst[pos.clamp(max=mm - 1)] == jt.to(torch.int32))).cpu().numpy()
+    v32 = ref.v.astype(np.float32)
+    want = oracle.bfasgd_decide(js, v32, c, 1e-8, SEED, ref.T, clients[K])
+    diff = got != want
+    if diff.any():
+        tv = v32[diff].astype(np.float64) + 1e-8
+        p = tv / (tv + c)
+        assert (np.abs(_philox_r(js[diff], SEED, ref.T, int(clients[K])) - p) <= 2 * RTOL_SEQ * p).all()
+        assert diff.sum() <= 4
+    sel = np.flatnonzero(want & ~diff)
+    sl = slice(K + 1, 2 * K + 1)
+    fa.fasgd_apply_with_push(st, idx, val, cnt, seg, clients[K], ts[K], grads[:K], clients[sl], ts[sl])
+    oracle.bfasgd_apply_sparse(ref, sel.astype(np.int32), g_host[K][sel], ts[K])
+    for k in range(K):
+        oracle.fasgd_apply(ref, g_host[k], ts[K + 1 + k])
+    torch.cuda.synchronize()
+    keep = np.flatnonzero(~diff)
+    assert_state_close(st, ref.take(keep), RTOL_SEQ, js=torch.from_numpy(js[keep]).to(dev),
+                       what="after the pass with the push")
+    assert st.T == 2 * K + 1 and st.dense_T == 2 * K
+    del grads, st, idx, val, ws, seg, lst
+    _free()
+
+
 def test_select_at_int32_index_limit():
     """P = 2^31 - 1, the largest B-FASGD size (int32 indices)."""
     import torch
