@@ -1,5 +1,6 @@
-// Dense server updates: state initialisation, the K-fused FASGD apply and
-// the K-fused SASGD apply.
+// Dense server updates: state initialisation, the K-fused FASGD apply (also
+// with a compacted B-FASGD push applied ahead of the K gradients in the same
+// pass), the K-fused SASGD apply and the synchronous-SGD step.
 //
 // Every update is elementwise and HBM-bound, so the kernels are plain
 // streaming passes: each thread owns 4 consecutive parameters (one 16-byte
