@@ -37,6 +37,7 @@ extern "C" {
 #endif
 
 #define FASGD_MAX_K 64          /* most gradients one fused apply accepts */
+#define FASGD_MAX_BATCH 64      /* most pushes one batched selection or apply accepts */
 
 typedef enum fasgd_status {
     FASGD_OK = 0,
@@ -202,6 +203,31 @@ fasgd_status bfasgd_select_compact(const fasgd_state* st, const float* grad, flo
 int64_t bfasgd_list_index_length(int64_t P);
 
 /*
+ * B pushes selected in one set of launches (Sec. 2.3): push b is exactly
+ * bfasgd_select_compact(st, grads[b], c, eps_c, seed, T[b], clients[b],
+ * out_idx + b capacity, out_val + b capacity, capacity, d_count + b,
+ * out_seg_start + b L, workspace slice b), with L =
+ * bfasgd_list_index_length(P): every push is decided from v as the state
+ * holds it at this call (the v its client last fetched, before any of the B
+ * pushes is applied).  For pushes that arrive at the server together, where
+ * one selection per push would be bound by launch latency.
+ *   B              1 .. FASGD_MAX_BATCH
+ *   grads          host array of B device pointers, each fp32 [P]
+ *   T, clients     host arrays [B]; each as for bfasgd_select_compact
+ *   out_idx, out_val  device [B][capacity]
+ *   d_count        device int64 [B]
+ *   out_seg_start  NULL, or device uint32 [B][L]
+ *   workspace      at least B * bfasgd_workspace_bytes(P) bytes, 256-byte aligned
+ * Errors: those of bfasgd_select_compact for any push, FASGD_ERR_ARG for B
+ * out of range; a rejected call enqueues nothing.
+ */
+fasgd_status bfasgd_select_compact_batch(const fasgd_state* st, int32_t B, const float* const* grads, float c,
+                                         float eps_c, uint64_t seed, const int64_t* T, const int32_t* clients,
+                                         int32_t* out_idx, float* out_val, int64_t capacity,
+                                         int64_t* d_count, uint32_t* out_seg_start,
+                                         void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Server side of a B-FASGD push: the FASGD update of fasgd_apply_updates,
  * applied at timestamp T with staleness T - grad_ts, to the listed
  * parameters only, with g = val[i] for parameter idx[i], for
@@ -245,6 +271,27 @@ fasgd_status fasgd_apply_with_push(fasgd_state* st, const int32_t* push_idx, con
                                    int64_t capacity, int32_t push_client, int64_t push_grad_ts,
                                    const float* const* grads, const int32_t* clients,
                                    const int64_t* grad_ts, int32_t K, hipStream_t stream);
+
+/*
+ * B compacted pushes applied in one pass (Sec. 2.3): the same state, T and
+ * last_T, bit for bit, as B calls of bfasgd_apply_sparse in order b = 0 ..
+ * B-1, push b at timestamp T + b with staleness T + b - grad_ts[b], but
+ * each parameter's state is read and written once.  A parameter listed by
+ * some push gets last_T = T + the last such b; T advances by B; dense_T is
+ * unchanged.
+ *   idx, val       device int32 / fp32 [B][capacity]; list b as
+ *                  bfasgd_select_compact writes it (ascending, distinct)
+ *   d_count        device int64 [B]
+ *   seg_start      device uint32 [B][bfasgd_list_index_length(P)], each
+ *                  list's index as bfasgd_select_compact writes it
+ *   clients, grad_ts  host arrays [B], as for bfasgd_apply_sparse
+ * Errors: those of the B calls it stands for; FASGD_ERR_ARG for B outside
+ * 1 .. FASGD_MAX_BATCH or T + B - 1 beyond INT32_MAX; FASGD_ERR_NULL for a
+ * NULL d_count or seg_start.
+ */
+fasgd_status fasgd_apply_pushes(fasgd_state* st, int32_t B, const int32_t* idx, const float* val,
+                                const int64_t* d_count, const uint32_t* seg_start, int64_t capacity,
+                                const int32_t* clients, const int64_t* grad_ts, hipStream_t stream);
 
 /*
  * Synchronous SGD server (Sec. 3, the apply-update listing): with the

@@ -22,6 +22,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libfasgd.so")
 
 FASGD_MAX_K = 64
+FASGD_MAX_BATCH = 64
 MATH_IEEE = 0
 MATH_FAST = 1
 V_EQUATIONS = 0     # v averages 1/sqrt(n - b^2 + eps) (Sec. 2.2's equation)
@@ -36,6 +37,7 @@ ABI_FUNCTIONS = ("fasgd_init_state", "fasgd_apply_updates", "sasgd_apply_updates
                  "sgd_sync_apply", "bfasgd_apply_cached", "bfasgd_apply_fetch",
                  "bfasgd_segments_workspace_bytes", "bfasgd_decide_segments", "bfasgd_apply_segments",
                  "bfasgd_list_index_length", "fasgd_apply_with_push",
+                 "bfasgd_select_compact_batch", "fasgd_apply_pushes",
                  "fasgd_status_string", "fasgd_last_error")
 
 
@@ -79,6 +81,8 @@ def load_library(path: Optional[str] = None):
     lib.bfasgd_list_index_length.restype = i64
     lib.fasgd_apply_with_push.argtypes = [S, P, P, P, P, i64, i32, i64, P, P, P, i32, P]
     lib.bfasgd_apply_sparse.argtypes = [S, P, P, P, i64, i32, i64, P]
+    lib.bfasgd_select_compact_batch.argtypes = [S, i32, P, f, f, u64, P, P, P, P, i64, P, P, P, sz, P]
+    lib.fasgd_apply_pushes.argtypes = [S, i32, P, P, P, P, i64, P, P, P]
     lib.sgd_sync_apply.argtypes = [S, P, f, P]
     lib.bfasgd_apply_cached.argtypes = [S, P, P, P, i64, P, i32, i64, P]
     lib.bfasgd_apply_fetch.argtypes = [P, i64, P, P, P, i64, P]
@@ -265,6 +269,75 @@ def fasgd_apply_with_push(state: State, push_idx, push_val, push_count, push_seg
         _dev_ptr(push_val, torch.float32, "push_val"), _dev_ptr(push_count, torch.int64, "push_count"),
         _seg_start_ptr(push_seg_start, state.P, required=True), cap, int(push_client), int(push_grad_ts),
         ptrs, c, t, K, _stream(stream))
+    _check(rc)
+
+
+def _batch_lists(B, out_idx, out_val, d_count):
+    """(capacity, B) of [B, capacity] list tensors and a [B] count tensor."""
+    if out_idx.dim() != 2 or out_idx.shape[0] != B or tuple(out_val.shape) != tuple(out_idx.shape):
+        raise ValueError(f"idx and val must both be [B = {B}, capacity]")
+    if d_count.numel() != B:
+        raise ValueError(f"d_count must have B = {B} entries")
+    return int(out_idx.shape[1])
+
+
+def _batch_seg(seg_start, B, P, required):
+    import torch
+    if seg_start is None and not required:
+        return None
+    L = bfasgd_list_index_length(P)
+    if seg_start is None or tuple(seg_start.shape) != (B, L):
+        raise ValueError(f"seg_start must be [B = {B}, bfasgd_list_index_length(P) = {L}]")
+    return _dev_ptr(seg_start, torch.int32, "seg_start")
+
+
+def bfasgd_select_compact_batch(state: State, grads: Sequence, c: float, eps_c: float, seed: int,
+                                T: Sequence[int], clients: Sequence[int], out_idx, out_val, d_count, workspace,
+                                seg_start=None, stream=None) -> None:
+    """B pushes selected in one set of launches, each exactly as
+    bfasgd_select_compact with its own gradient, T and client, all decided
+    from v as it stands now.  out_idx / out_val: [B, capacity]; d_count: [B];
+    seg_start (optional): int32 [B, bfasgd_list_index_length(P)]; workspace:
+    at least B * bfasgd_workspace_bytes(P) bytes."""
+    import torch
+    B = len(grads)
+    if len(T) != B or len(clients) != B:
+        raise ValueError("grads, T and clients must have the same length")
+    if not 1 <= B <= FASGD_MAX_BATCH:
+        raise ValueError(f"B = {B} is not in [1, {FASGD_MAX_BATCH}]")
+    cap = _batch_lists(B, out_idx, out_val, d_count)
+    ptrs = (ctypes.c_void_p * B)()
+    for k, g in enumerate(grads):
+        if g.numel() != state.P:
+            raise ValueError(f"grads[{k}] has {g.numel()} elements, P = {state.P}")
+        ptrs[k] = _dev_ptr(g, torch.float32, f"grads[{k}]")
+    ts = (ctypes.c_int64 * B)(*[int(x) for x in T])
+    cl = (ctypes.c_int32 * B)(*[int(x) for x in clients])
+    rc = load_library().bfasgd_select_compact_batch(
+        ctypes.byref(state.c), B, ptrs, c, eps_c, int(seed) & (2 ** 64 - 1), ts, cl,
+        _dev_ptr(out_idx, torch.int32, "out_idx"), _dev_ptr(out_val, torch.float32, "out_val"), cap,
+        _dev_ptr(d_count, torch.int64, "d_count"), _batch_seg(seg_start, B, state.P, False),
+        _dev_ptr(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
+    _check(rc)
+
+
+def fasgd_apply_pushes(state: State, idx, val, d_count, seg_start, clients: Sequence[int], grad_ts: Sequence[int],
+                       stream=None) -> None:
+    """B compacted pushes ([B, capacity] lists with their [B, L] index) in one
+    pass, as B bfasgd_apply_sparse calls in order; T advances by B."""
+    import torch
+    B = len(clients)
+    if len(grad_ts) != B:
+        raise ValueError("clients and grad_ts must have the same length")
+    if not 1 <= B <= FASGD_MAX_BATCH:
+        raise ValueError(f"B = {B} is not in [1, {FASGD_MAX_BATCH}]")
+    cap = _batch_lists(B, idx, val, d_count)
+    cl = (ctypes.c_int32 * B)(*[int(x) for x in clients])
+    ts = (ctypes.c_int64 * B)(*[int(x) for x in grad_ts])
+    rc = load_library().fasgd_apply_pushes(
+        ctypes.byref(state.c), B, _dev_ptr(idx, torch.int32, "idx"), _dev_ptr(val, torch.float32, "val"),
+        _dev_ptr(d_count, torch.int64, "d_count"), _batch_seg(seg_start, B, state.P, True), cap, cl, ts,
+        _stream(stream))
     _check(rc)
 
 

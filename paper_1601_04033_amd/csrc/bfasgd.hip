@@ -69,6 +69,30 @@ __device__ __forceinline__ int64_t wave_tile()
     return static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
 }
 
+// The arguments of push blockIdx.y of a batch: its gradient, counter words,
+// list, count, list index and workspace slice.
+__device__ __forceinline__ SelectArgs push_args(const SelectArgs& a0, const SelectBatch& bt)
+{
+    const int b = blockIdx.y;
+    if (b == 0) return a0;
+    SelectArgs a = a0;
+    a.grad = bt.grad[b];
+    a.ctr_T = bt.ctr_T[b];
+    a.ctr_client = bt.ctr_client[b];
+    if (a0.out_idx) a.out_idx = a0.out_idx + b * bt.list_stride;
+    if (a0.out_val) a.out_val = a0.out_val + b * bt.list_stride;
+    a.d_count = a0.d_count + b;
+    if (a0.seg_start) a.seg_start = a0.seg_start + b * bt.index_stride;
+    const size_t off = b * bt.ws_stride;
+    a.ballots = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(a0.ballots) + off);
+    a.tile_count = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(a0.tile_count) + off);
+    a.tile_offset = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(a0.tile_offset) + off);
+    a.group_total = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(a0.group_total) + off);
+    a.group_offset = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(a0.group_offset) + off);
+    a.groups_done = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(a0.groups_done) + off);
+    return a;
+}
+
 // Mark one tile.  FULL: the tile lies inside [0, P) and v is 16-byte
 // aligned, so no lane needs a bounds check (every tile but the last).
 template <bool FULL>
@@ -116,8 +140,9 @@ __device__ __forceinline__ void mark_tile(const SelectArgs& a, int64_t tile, int
     if (lane == 0) a.tile_count[tile] = count;
 }
 
-__global__ __launch_bounds__(kSelBlock) void select_mark(const SelectArgs a, bool aligned)
+__global__ __launch_bounds__(kSelBlock) void select_mark(const SelectArgs a0, const SelectBatch bt, bool aligned)
 {
+    const SelectArgs a = push_args(a0, bt);
     if (blockIdx.x == 0 && threadIdx.x == 0) *a.groups_done = 0u;   // for the scan launch
     const int64_t tile = wave_tile();
     if (tile >= a.n_tiles) return;
@@ -185,8 +210,9 @@ __device__ __forceinline__ void scan_groups(const SelectArgs& a, int64_t ng, boo
 // Each arrival is a device-scope release, which costs more than a launch once
 // there are many groups; then select_top does that scan as its own launch.
 template <bool FUSED_TOP>
-__global__ __launch_bounds__(kScanBlock) void select_scan(const SelectArgs a)
+__global__ __launch_bounds__(kScanBlock) void select_scan(const SelectArgs a0, const SelectBatch bt)
 {
+    const SelectArgs a = push_args(a0, bt);
     const int64_t t = static_cast<int64_t>(blockIdx.x) * kScanBlock + threadIdx.x;
     const uint32_t c = t < a.n_tiles ? a.tile_count[t] : 0u;
     uint32_t total;
@@ -207,8 +233,9 @@ __global__ __launch_bounds__(kScanBlock) void select_scan(const SelectArgs a)
     if (last) scan_groups(a, gridDim.x, true);
 }
 
-__global__ __launch_bounds__(kScanBlock) void select_top(const SelectArgs a)
+__global__ __launch_bounds__(kScanBlock) void select_top(const SelectArgs a0, const SelectBatch bt)
 {
+    const SelectArgs a = push_args(a0, bt);
     scan_groups(a, (a.n_tiles + kScanBlock - 1) / kScanBlock, false);
 }
 
@@ -303,8 +330,9 @@ __device__ __forceinline__ void scatter_tile(const SelectArgs& a, int64_t tile, 
     }
 }
 
-__global__ __launch_bounds__(kSelBlock) void select_scatter(const SelectArgs a, bool aligned)
+__global__ __launch_bounds__(kSelBlock) void select_scatter(const SelectArgs a0, const SelectBatch bt, bool aligned)
 {
+    const SelectArgs a = push_args(a0, bt);
     __shared__ int32_t s_idx[kWavesPerBlock][kStageEntries];
     __shared__ float s_val[kWavesPerBlock][kStageEntries];
     const int64_t tile = wave_tile();
@@ -402,25 +430,26 @@ void select_workspace_layout(void* ws, int64_t P, SelectArgs& a)
     a.n_tiles = nt;
 }
 
-hipError_t launch_select(const SelectArgs& a, bool aligned, hipStream_t s)
+hipError_t launch_select(const SelectArgs& a, const SelectBatch& bt, int B, bool aligned, hipStream_t s)
 {
-    const unsigned grid = static_cast<unsigned>((a.n_tiles + kWavesPerBlock - 1) / kWavesPerBlock);
+    const unsigned gx = static_cast<unsigned>((a.n_tiles + kWavesPerBlock - 1) / kWavesPerBlock);
     const unsigned groups = static_cast<unsigned>((a.n_tiles + kScanBlock - 1) / kScanBlock);
-    if (groups > static_cast<unsigned>(kMaxGroups)) return hipErrorInvalidValue;
-    select_mark<<<grid, kSelBlock, 0, s>>>(a, aligned);
+    if (groups > static_cast<unsigned>(kMaxGroups) || B < 1 || B > kMaxBatch) return hipErrorInvalidValue;
+    const dim3 grid(gx, static_cast<unsigned>(B));
+    select_mark<<<grid, kSelBlock, 0, s>>>(a, bt, aligned);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (groups <= static_cast<unsigned>(kFusedTopGroups)) {
-        select_scan<true><<<groups, kScanBlock, 0, s>>>(a);
+        select_scan<true><<<dim3(groups, B), kScanBlock, 0, s>>>(a, bt);
     } else {
-        select_scan<false><<<groups, kScanBlock, 0, s>>>(a);
+        select_scan<false><<<dim3(groups, B), kScanBlock, 0, s>>>(a, bt);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
-        select_top<<<1, kScanBlock, 0, s>>>(a);
+        select_top<<<dim3(1, B), kScanBlock, 0, s>>>(a, bt);
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    select_scatter<<<grid, kSelBlock, 0, s>>>(a, aligned);
+    select_scatter<<<grid, kSelBlock, 0, s>>>(a, bt, aligned);
     return hipGetLastError();
 }
 

@@ -9,6 +9,7 @@
 #include "kernels.hpp"
 
 static_assert(FASGD_MAX_K == fasgd::kMaxK, "K limit mismatch");
+static_assert(FASGD_MAX_BATCH == fasgd::kMaxBatch, "batch limit mismatch");
 
 namespace {
 
@@ -240,35 +241,56 @@ int64_t bfasgd_list_index_length(int64_t P)
     return fasgd::push_segments(P) + 1;
 }
 
-fasgd_status bfasgd_select_compact(const fasgd_state* st, const float* grad, float c, float eps_c, uint64_t seed,
-                                   int64_t T, int32_t client, int32_t* out_idx, float* out_val, int64_t capacity,
-                                   int64_t* d_count, uint32_t* out_seg_start, void* workspace,
-                                   size_t workspace_bytes, hipStream_t stream)
+namespace {
+
+// Checks and launch of B selections; push b's per-push arguments are
+// grads[b], T[b], clients[b].
+fasgd_status select_common(const fasgd_state* st, int32_t B, const float* const* grads, float c, float eps_c,
+                           uint64_t seed, const int64_t* T, const int32_t* clients, int32_t* out_idx,
+                           float* out_val, int64_t capacity, int64_t* d_count, uint32_t* out_seg_start,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream, const char* what)
 {
     if (!st) return fail(FASGD_ERR_NULL, "state is NULL");
     if (st->P < 1 || st->P > INT32_MAX) return fail(FASGD_ERR_ARG, "P must be in [1, INT32_MAX] for int32 indices");
     if (st->lambda < 1) return fail(FASGD_ERR_ARG, "lambda = %d must be >= 1", st->lambda);
-    if (!st->v || !grad || !d_count || !workspace) return fail(FASGD_ERR_NULL, "v, grad, d_count or workspace is NULL");
+    if (B < 1 || B > FASGD_MAX_BATCH) return fail(FASGD_ERR_ARG, "B = %d is not in [1, %d]", B, FASGD_MAX_BATCH);
+    if (!st->v || !grads || !T || !clients || !d_count || !workspace)
+        return fail(FASGD_ERR_NULL, "v, grad, T, clients, d_count or workspace is NULL");
     if (capacity < 0) return fail(FASGD_ERR_ARG, "capacity must be >= 0");
     if (capacity > 0 && (!out_idx || !out_val)) return fail(FASGD_ERR_NULL, "out_idx or out_val is NULL");
     if (!finite_nonneg(c) || !finite_nonneg(eps_c)) return fail(FASGD_ERR_ARG, "c and eps_c must be finite and >= 0");
-    if (T < 0 || T > int64_t(UINT32_MAX)) return fail(FASGD_ERR_ARG, "T = %lld is not in [0, 2^32)", (long long)T);
-    if (client < 0 || client >= st->lambda)
-        return fail(FASGD_ERR_CLIENT, "client = %d is outside [0, %d)", client, st->lambda);
-    if (!aligned(st->v, 4) || !aligned(grad, 4) || (out_idx && !aligned(out_idx, 4)) ||
-        (out_val && !aligned(out_val, 4)) || !aligned(d_count, 8) || (out_seg_start && !aligned(out_seg_start, 4)))
+    for (int32_t p = 0; p < B; ++p) {
+        if (!grads[p]) return fail(FASGD_ERR_NULL, "grad of push %d is NULL", p);
+        if (T[p] < 0 || T[p] > int64_t(UINT32_MAX))
+            return fail(FASGD_ERR_ARG, "T = %lld (push %d) is not in [0, 2^32)", (long long)T[p], p);
+        if (clients[p] < 0 || clients[p] >= st->lambda)
+            return fail(FASGD_ERR_CLIENT, "client = %d (push %d) is outside [0, %d)", clients[p], p, st->lambda);
+        if (!aligned(grads[p], 4)) return fail(FASGD_ERR_ALIGN, "misaligned grad (push %d)", p);
+    }
+    if (!aligned(st->v, 4) || (out_idx && !aligned(out_idx, 4)) || (out_val && !aligned(out_val, 4)) ||
+        !aligned(d_count, 8) || (out_seg_start && !aligned(out_seg_start, 4)))
         return fail(FASGD_ERR_ALIGN, "misaligned v, grad, output list, d_count or out_seg_start");
     if (!aligned(workspace, 256)) return fail(FASGD_ERR_ALIGN, "workspace must be 256-byte aligned");
     if (st->index_base < 0 || (st->index_base & 3) != 0 || st->index_base > (int64_t(1) << 62) - st->P)
         return fail(FASGD_ERR_ARG, "index_base = %lld must be a multiple of 4 in [0, 2^62 - P]",
                     (long long)st->index_base);
-    if (workspace_bytes < fasgd::select_workspace_bytes(st->P))
+    const size_t per_push = fasgd::select_workspace_bytes(st->P);
+    if (workspace_bytes / size_t(B) < per_push)
         return fail(FASGD_ERR_CAPACITY, "workspace of %zu bytes is smaller than the %zu needed", workspace_bytes,
-                    fasgd::select_workspace_bytes(st->P));
+                    per_push * size_t(B));
     fasgd::SelectArgs a;
     memset(&a, 0, sizeof a);
+    fasgd::SelectBatch bt;
+    memset(&bt, 0, sizeof bt);
+    bool vec = aligned(st->v, 16);
+    for (int32_t p = 0; p < B; ++p) {
+        bt.grad[p] = grads[p];
+        bt.ctr_T[p] = static_cast<uint32_t>(T[p]);
+        bt.ctr_client[p] = static_cast<uint32_t>(clients[p]);
+        vec = vec && aligned(grads[p], 16);
+    }
     a.v = st->v;
-    a.grad = grad;
+    a.grad = grads[0];
     a.out_idx = out_idx;
     a.out_val = out_val;
     a.d_count = d_count;
@@ -278,16 +300,39 @@ fasgd_status bfasgd_select_compact(const fasgd_state* st, const float* grad, flo
     a.eps_c = eps_c;
     a.key0 = static_cast<uint32_t>(seed);
     a.key1 = static_cast<uint32_t>(seed >> 32);
-    a.ctr_T = static_cast<uint32_t>(T);
-    a.ctr_client = static_cast<uint32_t>(client);
+    a.ctr_T = bt.ctr_T[0];
+    a.ctr_client = bt.ctr_client[0];
     a.chunk_base = static_cast<uint64_t>(st->index_base) >> 2;
     a.seg_start = out_seg_start;
     a.n_segs = fasgd::push_segments(st->P);
     fasgd::select_workspace_layout(workspace, st->P, a);
-    const bool vec = aligned(st->v, 16) && aligned(grad, 16);
-    const hipError_t e = fasgd::launch_select(a, vec, stream);
-    if (e != hipSuccess) return hip_fail(e, "bfasgd_select_compact");
+    bt.list_stride = capacity;
+    bt.index_stride = a.n_segs + 1;
+    bt.ws_stride = per_push;
+    const hipError_t e = fasgd::launch_select(a, bt, B, vec, stream);
+    if (e != hipSuccess) return hip_fail(e, what);
     return ok();
+}
+
+}  // namespace
+
+fasgd_status bfasgd_select_compact(const fasgd_state* st, const float* grad, float c, float eps_c, uint64_t seed,
+                                   int64_t T, int32_t client, int32_t* out_idx, float* out_val, int64_t capacity,
+                                   int64_t* d_count, uint32_t* out_seg_start, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream)
+{
+    return select_common(st, 1, &grad, c, eps_c, seed, &T, &client, out_idx, out_val, capacity, d_count,
+                         out_seg_start, workspace, workspace_bytes, stream, "bfasgd_select_compact");
+}
+
+fasgd_status bfasgd_select_compact_batch(const fasgd_state* st, int32_t B, const float* const* grads, float c,
+                                         float eps_c, uint64_t seed, const int64_t* T, const int32_t* clients,
+                                         int32_t* out_idx, float* out_val, int64_t capacity, int64_t* d_count,
+                                         uint32_t* out_seg_start, void* workspace, size_t workspace_bytes,
+                                         hipStream_t stream)
+{
+    return select_common(st, B, grads, c, eps_c, seed, T, clients, out_idx, out_val, capacity, d_count,
+                         out_seg_start, workspace, workspace_bytes, stream, "bfasgd_select_compact_batch");
 }
 
 fasgd_status bfasgd_apply_sparse(fasgd_state* st, const int32_t* idx, const float* val, const int64_t* d_count,
@@ -362,6 +407,53 @@ fasgd_status fasgd_apply_with_push(fasgd_state* st, const int32_t* push_idx, con
     if (e != hipSuccess) return hip_fail(e, "fasgd_apply_with_push");
     st->dense_T = st->T + K;
     st->T += K + 1;
+    return ok();
+}
+
+fasgd_status fasgd_apply_pushes(fasgd_state* st, int32_t B, const int32_t* idx, const float* val,
+                                const int64_t* d_count, const uint32_t* seg_start, int64_t capacity,
+                                const int32_t* clients, const int64_t* grad_ts, hipStream_t stream)
+{
+    fasgd_status s = check_state(st, true);
+    if (s != FASGD_OK) return s;
+    if (B < 1 || B > FASGD_MAX_BATCH) return fail(FASGD_ERR_ARG, "B = %d is not in [1, %d]", B, FASGD_MAX_BATCH);
+    if (st->P > INT32_MAX) return fail(FASGD_ERR_ARG, "P must be <= INT32_MAX for int32 indices");
+    if (st->T + B - 1 > INT32_MAX) return fail(FASGD_ERR_ARG, "T + B - 1 exceeds the int32 timestamp range");
+    if (!d_count || !seg_start || !clients || !grad_ts)
+        return fail(FASGD_ERR_NULL, "d_count, seg_start, clients or grad_ts is NULL");
+    if (capacity < 0) return fail(FASGD_ERR_ARG, "capacity must be >= 0");
+    if (capacity > 0 && (!idx || !val)) return fail(FASGD_ERR_NULL, "idx or val is NULL");
+    if ((idx && !aligned(idx, 4)) || (val && !aligned(val, 4)) || !aligned(d_count, 8) || !aligned(seg_start, 4))
+        return fail(FASGD_ERR_ALIGN, "misaligned idx, val, d_count or seg_start");
+    float tau_div[FASGD_MAX_BATCH];
+    s = staleness(st, clients, grad_ts, B, tau_div);
+    if (s != FASGD_OK) return s;
+    if (capacity > 0) {
+        fasgd::PushBatchArgs a;
+        memset(&a, 0, sizeof a);
+        a.theta = st->theta;
+        a.n = st->n;
+        a.b = st->b;
+        a.v = st->v;
+        a.last_T = st->last_T;
+        a.idx = idx;
+        a.val = val;
+        a.d_count = d_count;
+        a.seg_start = seg_start;
+        a.list_stride = capacity;
+        a.n_segs = fasgd::push_segments(st->P);
+        a.P = st->P;
+        a.B = B;
+        a.T0 = static_cast<int32_t>(st->T);
+        for (int32_t p = 0; p < B; ++p)
+            a.coef[p] = st->math_mode == FASGD_MATH_FAST ? st->alpha / tau_div[p] : tau_div[p];
+        a.h = hyper_of(st);
+        const bool vec = aligned(st->theta, 16) && aligned(st->n, 16) && aligned(st->b, 16) &&
+                         aligned(st->v, 16) && aligned(st->last_T, 16);
+        const hipError_t e = fasgd::launch_apply_pushes(a, variant_of(st), vec, stream);
+        if (e != hipSuccess) return hip_fail(e, "fasgd_apply_pushes");
+    }
+    st->T += B;
     return ok();
 }
 

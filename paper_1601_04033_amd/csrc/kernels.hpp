@@ -61,10 +61,22 @@ struct SelectArgs {
     int64_t n_segs;
 };
 
+// Several pushes selected in one set of launches (the grid's y index is the
+// push): SelectArgs describes push 0 and SelectBatch how the others differ.
+constexpr int kMaxBatch = 64;
+struct SelectBatch {
+    const float* grad[kMaxBatch];
+    uint32_t ctr_T[kMaxBatch];
+    uint32_t ctr_client[kMaxBatch];
+    int64_t list_stride;    // entries between consecutive pushes' lists (their capacity)
+    int64_t index_stride;   // entries between consecutive pushes' list indexes
+    size_t ws_stride;       // workspace bytes per push
+};
+
 size_t select_workspace_bytes(int64_t P);
 // Carve the workspace into ballots / tile counts / tile offsets.
 void select_workspace_layout(void* ws, int64_t P, SelectArgs& a);
-hipError_t launch_select(const SelectArgs& a, bool aligned, hipStream_t s);
+hipError_t launch_select(const SelectArgs& a, const SelectBatch& bt, int B, bool aligned, hipStream_t s);
 
 struct SparseArgs {
     float* theta;
@@ -102,6 +114,29 @@ struct PushArgs {
 
 hipError_t launch_fasgd_dense_push(const DenseArgs& a, const PushArgs& p, int variant, bool aligned,
                                    hipStream_t s);
+
+// B compacted pushes applied in order in one pass (push b at timestamp
+// T0 + b); listed parameters get last_T = T0 + the last push that lists them.
+struct PushBatchArgs {
+    float* theta;
+    float* n;
+    float* b;
+    float* v;
+    int32_t* last_T;
+    const int32_t* idx;        // [B][list_stride]
+    const float* val;          // [B][list_stride]
+    const int64_t* d_count;    // [B]
+    const uint32_t* seg_start; // [B][n_segs + 1]
+    int64_t list_stride;       // the lists' capacity
+    int64_t n_segs;
+    int64_t P;
+    int32_t B;
+    int32_t T0;
+    float coef[kMaxBatch];
+    Hyper h;
+};
+
+hipError_t launch_apply_pushes(const PushBatchArgs& a, int variant, bool aligned, hipStream_t s);
 
 // Paper-literal decisions per segment (groups of up to kSegGroup segments).
 constexpr int kSegGroup = 32;

@@ -228,6 +228,67 @@ def test_fused_push_rejects_bad_arguments(lib):
     assert st.T == 2 and st.dense_T == -1
 
 
+def test_batch_select_rejects_bad_arguments(lib):
+    """The batched selection checks every push's arguments and the workspace
+    for all B pushes; B is in 1 .. FASGD_MAX_BATCH."""
+    st, f = _state(P=16)
+    ws_need = fa.bfasgd_workspace_bytes(16)
+    ws = np.zeros(3 * ws_need + 512, np.uint8)
+    wsp = (ws.ctypes.data + 255) & ~255
+    cnt = np.zeros(4, np.int64)
+    cntp = (cnt.ctypes.data + 7) & ~7
+
+    def sel(B=3, T=(0, 1, 2), clients=(0, 1, 2), grads=None, ws_bytes=3 * ws_need, cap=16):
+        n = max(B, 1)
+        g = (ctypes.c_void_p * n)(*(grads or [f.ptr(5)] * n))
+        t = (ctypes.c_int64 * n)(*(list(T) + [0] * n)[:n])
+        c = (ctypes.c_int32 * n)(*(list(clients) + [0] * n)[:n])
+        return lib.bfasgd_select_compact_batch(ctypes.byref(st), B, g, 1.0, 1e-8, 7, t, c, f.ptr(0), f.ptr(1),
+                                               cap, cntp, None, wsp, ws_bytes, None)
+
+    assert sel(B=0) == 2
+    assert sel(B=fa.FASGD_MAX_BATCH + 1) == 2
+    assert sel(T=(0, -1, 2)) == 2
+    assert sel(clients=(0, 1, 4)) == 4
+    assert sel(grads=[f.ptr(5), None, f.ptr(5)]) == 1
+    assert sel(grads=[f.ptr(5), f.ptr(5), f.ptr(5, misalign=2)]) == 5
+    assert sel(ws_bytes=3 * ws_need - 1) == 6
+    assert sel(cap=-1) == 2
+    assert lib.bfasgd_select_compact_batch(ctypes.byref(st), 1, None, 1.0, 1e-8, 7, None, None, f.ptr(0),
+                                           f.ptr(1), 16, cntp, None, wsp, ws_need, None) == 1
+
+
+def test_apply_pushes_rejects_bad_arguments(lib):
+    """The batched apply: push b is applied at T + b, so grad_ts[b] may be
+    at most T + b; a rejected call leaves T alone."""
+    st, f = _state(P=16, T=2)
+    cnt = np.zeros(4, np.int64)
+    cntp = (cnt.ctypes.data + 7) & ~7
+
+    def ap(B=2, ts=(2, 3), clients=(0, 1), cap=16, count=cntp, seg="ok"):
+        n = max(B, 1)
+        t = (ctypes.c_int64 * n)(*(list(ts) + [0] * n)[:n])
+        c = (ctypes.c_int32 * n)(*(list(clients) + [0] * n)[:n])
+        segp = f.ptr(3) if seg == "ok" else seg
+        return lib.fasgd_apply_pushes(ctypes.byref(st), B, f.ptr(0), f.ptr(1), count, segp, cap, c, t, None)
+
+    assert ap(B=0) == 2
+    assert ap(B=fa.FASGD_MAX_BATCH + 1) == 2
+    assert ap(ts=(3, 3)) == 3            # push 0 is applied at T = 2
+    assert ap(ts=(2, 4)) == 3            # push 1 at T + 1 = 3
+    assert ap(clients=(0, 4)) == 4
+    assert ap(count=None) == 1
+    assert ap(seg=None) == 1
+    assert ap(seg=f.ptr(3, misalign=2)) == 5
+    assert ap(count=cntp + 4) == 5
+    assert ap(cap=-1) == 2
+    st.T = 2 ** 31 - 1
+    assert ap(ts=(0, 0), cap=0) == 2     # T + B - 1 beyond INT32_MAX
+    assert st.T == 2 ** 31 - 1
+    st.T = 2
+    assert ap(cap=0) == 0 and st.T == 4  # nothing to apply: T still advances by B
+
+
 def test_sparse_rejects_bad_arguments(lib):
     st, f = _state(P=16, T=2)
     cnt = np.zeros(2, np.int64)

@@ -1,0 +1,223 @@
+"""GPU checks of B-FASGD pushes handled in batches: bfasgd_select_compact_batch
+(B selections in one set of launches) gives, push by push, the counts,
+lists and list indexes of B single bfasgd_select_compact calls bit for bit
+and the oracle's; fasgd_apply_pushes (B compacted pushes in one pass) gives
+theta, n, b, v, last_T and T bit for bit as B bfasgd_apply_sparse calls in
+order, and the oracle's state within the sequence tolerance."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1601_04033_amd as fa
+import workload
+from helpers import RTOL_SEQ, assert_state_close, gpu, to_dev
+
+pytestmark = pytest.mark.gpu
+SEED = 0xBA7C4
+
+
+def _mid_run_state(P, dev, mode=fa.MATH_FAST, reading=fa.V_EQUATIONS, seed=0, offset=0, T=40, copies=2):
+    """`copies` identical mid-run GPU states (synthetic n, b, v, theta; T = 40,
+    last_T partly set) and the oracle state holding the same values;
+    offset = 1 places the arrays 4 bytes into their buffers (scalar paths)."""
+    import torch
+    w = workload.WORKLOADS["mlp_bfasgd" if P <= workload.MLP_P else "large"]
+    theta0, m_, s_ = workload.host_params(w, P, seed=seed)
+    b0 = m_ + s_ * np.float32(0.1)
+    n0 = (b0 * b0 + s_ * s_).astype(np.float32)
+    v0 = workload.synthetic_v(P, seed=seed, lo=5.0, hi=100.0)
+    lt0 = np.where(np.arange(P) % 3 == 0, T - 7, -1).astype(np.int32)
+    out = []
+    for _ in range(copies):
+        bufs = fa.allocate_state(P + offset, dev)
+        theta, n, b, v, last_T = (t[offset:] for t in bufs)
+        st = fa.fasgd_init_state(theta, n, b, v, last_T, lam=w.lam, alpha=w.alpha_fasgd, math_mode=mode,
+                                 v_reading=reading)
+        for t, a in ((theta, theta0), (n, n0), (b, b0), (v, v0), (last_T, lt0)):
+            t.copy_(torch.from_numpy(a))
+        st.c.T = T
+        out.append((st, bufs))
+    ref = oracle.init_state(theta0, alpha=w.alpha_fasgd, v_reading=reading)
+    ref.n, ref.b, ref.v = n0.astype(np.float64), b0.astype(np.float64), v0.astype(np.float64)
+    ref.last_T = lt0.astype(np.int64)
+    ref.T = T
+    return [o[0] for o in out], ref, (m_, s_, w), [o[1] for o in out]
+
+
+def _gradients(B, P, m_, s_, w, dev, seed, offset=0):
+    import torch
+    out = []
+    for k in range(B):
+        g = workload.host_gradient(w, m_, s_, 100 + k, seed=seed)
+        if offset:
+            buf = torch.empty(P + offset, device=dev)
+            buf[offset:].copy_(torch.from_numpy(g))
+            out.append(buf[offset:])
+        else:
+            out.append(to_dev(g, dev))
+    return out
+
+
+def _batch_buffers(B, P, cap, dev):
+    import torch
+    idx = torch.full((B, cap), -1, device=dev, dtype=torch.int32)
+    val = torch.zeros((B, cap), device=dev)
+    cnt = torch.zeros(B, device=dev, dtype=torch.int64)
+    seg = torch.full((B, fa.bfasgd_list_index_length(P)), -1, device=dev, dtype=torch.int32)
+    ws = torch.empty(B * fa.bfasgd_workspace_bytes(P), device=dev, dtype=torch.uint8)
+    return idx, val, cnt, seg, ws
+
+
+@pytest.mark.parametrize("P,B,cap_frac,offset", [
+    (1, 3, 1.0, 0), (1027, 16, 1.0, 0), (100_003, 16, 1.0, 0), (100_003, 5, 0.05, 0),
+    (1_000_003, 64, 1.0, 0), (65_537, 7, 1.0, 1), (17_000_003, 3, 1.0, 0)])
+def test_batch_select_equals_single_selects(P, B, cap_frac, offset):
+    """Push by push, the batch gives the count, list and list index of a
+    single selection with the same gradient, T and client, bit for bit
+    (including a capacity cut, the scalar path for gradients 4 bytes off
+    16-byte alignment, 64 pushes, and 17M parameters, where the group scan
+    takes its two-launch form)."""
+    import torch
+    dev = gpu()
+    (st,), _, (m_, s_, w), keep = _mid_run_state(P, dev, seed=P % 977, copies=1)
+    grads = _gradients(B, P, m_, s_, w, dev, seed=5, offset=offset)
+    Ts = [40 + 3 * k for k in range(B)]
+    clients = [(5 * k + 1) % w.lam for k in range(B)]
+    cap = max(1, int(P * cap_frac))
+    idx, val, cnt, seg, ws = _batch_buffers(B, P, cap, dev)
+    fa.bfasgd_select_compact_batch(st, grads, 60.0, 1e-8, SEED, Ts, clients, idx, val, cnt, ws, seg_start=seg)
+    one_ws = fa.allocate_workspace(P, dev)
+    for k in range(B):
+        i1 = torch.full((cap,), -1, device=dev, dtype=torch.int32)
+        v1 = torch.zeros(cap, device=dev)
+        c1 = torch.zeros(1, device=dev, dtype=torch.int64)
+        s1 = torch.full((fa.bfasgd_list_index_length(P),), -1, device=dev, dtype=torch.int32)
+        fa.bfasgd_select_compact(st, grads[k], 60.0, 1e-8, SEED, Ts[k], clients[k], i1, v1, c1, one_ws,
+                                 seg_start=s1)
+        torch.cuda.synchronize()
+        m = int(c1.item())
+        assert int(cnt[k].item()) == m, k
+        u = min(m, cap)
+        assert torch.equal(idx[k, :u], i1[:u]), k
+        assert torch.equal(val[k, :u].view(torch.int32), v1[:u].view(torch.int32)), k
+        assert torch.equal(seg[k], s1), k
+        if cap_frac == 1.0:
+            assert (idx[k, u:] == -1).all(), "nothing is written past the count"
+
+
+def test_batch_select_matches_oracle():
+    """Every push of a batch against the oracle's selection from the same v."""
+    import torch
+    dev = gpu()
+    P, B = 300_007, 8
+    (st,), ref, (m_, s_, w), keep = _mid_run_state(P, dev, seed=31, copies=1)
+    grads_h = [workload.host_gradient(w, m_, s_, 100 + k, seed=31) for k in range(B)]
+    Ts, clients = [40 + k for k in range(B)], [k % w.lam for k in range(B)]
+    idx, val, cnt, seg, ws = _batch_buffers(B, P, P, dev)
+    fa.bfasgd_select_compact_batch(st, [to_dev(g, dev) for g in grads_h], 80.0, 1e-8, SEED, Ts, clients,
+                                   idx, val, cnt, ws, seg_start=seg)
+    torch.cuda.synchronize()
+    v32 = ref.v.astype(np.float32)
+    for k in range(B):
+        r_idx, r_val, r_m = oracle.bfasgd_select(v32, grads_h[k], 80.0, 1e-8, SEED, Ts[k], clients[k])
+        assert int(cnt[k].item()) == r_m
+        np.testing.assert_array_equal(idx[k, :r_m].cpu().numpy(), r_idx)
+        np.testing.assert_array_equal(val[k, :r_m].cpu().numpy().view(np.int32),
+                                      np.asarray(r_val, np.float32).view(np.int32))
+        assert 0.02 < r_m / P < 0.5
+
+
+def _lists_from_singles(st, grads, cs, Ts, clients, cap, dev):
+    """[B, cap] lists built from single selections with a threshold per push
+    (the batched call shares one c)."""
+    import torch
+    B, P = len(grads), st.P
+    idx, val, cnt, seg, _ = _batch_buffers(B, P, cap, dev)
+    ws = fa.allocate_workspace(P, dev)
+    for k in range(B):
+        fa.bfasgd_select_compact(st, grads[k], cs[k], 1e-8, SEED, Ts[k], clients[k], idx[k], val[k],
+                                 cnt[k:k + 1], ws, seg_start=seg[k])
+    return idx, val, cnt, seg
+
+
+def _assert_same(a, b):
+    import torch
+    torch.cuda.synchronize()
+    for name in ("theta", "n", "b", "v", "last_T"):
+        assert torch.equal(a.tensors[name].view(torch.int32), b.tensors[name].view(torch.int32)), name
+    assert a.T == b.T and a.dense_T == b.dense_T
+
+
+@pytest.mark.parametrize("reading", [fa.V_EQUATIONS, fa.V_PROSE])
+@pytest.mark.parametrize("mode", [fa.MATH_FAST, fa.MATH_IEEE])
+@pytest.mark.parametrize("P,B,offset", [(1, 2, 0), (255, 3, 0), (257, 9, 0), (100_003, 16, 0),
+                                        (1_000_003, 64, 0), (65_537, 5, 1)])
+def test_apply_pushes_is_bit_identical(P, B, offset, mode, reading):
+    """B pushes at about 20 % from a batched selection: one fasgd_apply_pushes
+    gives the state, last_T and T of B bfasgd_apply_sparse calls in order,
+    bit for bit (vector path with a ragged tail, and the scalar path for
+    arrays 4 bytes off 16-byte alignment)."""
+    dev = gpu()
+    (a, b), _, (m_, s_, w), keep = _mid_run_state(P, dev, mode, reading, seed=P % 1013, offset=offset)
+    grads = _gradients(B, P, m_, s_, w, dev, seed=9)
+    Ts = [40 + k for k in range(B)]
+    clients = [k % w.lam for k in range(B)]
+    grad_ts = [max(40 + k - (k % 5) - 1, 0) for k in range(B)]
+    idx, val, cnt, seg, ws = _batch_buffers(B, P, P, dev)
+    fa.bfasgd_select_compact_batch(a, grads, 60.0, 1e-8, SEED, Ts, clients, idx, val, cnt, ws, seg_start=seg)
+    for k in range(B):
+        fa.bfasgd_apply_sparse(a, idx[k], val[k], cnt[k:k + 1], clients[k], grad_ts[k])
+    fa.fasgd_apply_pushes(b, idx, val, cnt, seg, clients, grad_ts)
+    _assert_same(a, b)
+    assert b.T == 40 + B
+
+
+@pytest.mark.parametrize("case", ["mixed", "all_every_push", "truncated", "nothing"])
+def test_apply_pushes_edge_lists(case):
+    """Pushes of everything (more than 64 entries per 256 parameters), of
+    nothing, lists cut by capacity, and a mix of these in one batch."""
+    import torch
+    dev = gpu()
+    P, B = 200_003, 6
+    (a, b), _, (m_, s_, w), keep = _mid_run_state(P, dev, seed=3)
+    grads = _gradients(B, P, m_, s_, w, dev, seed=3)
+    Ts, clients = [40 + k for k in range(B)], [k for k in range(B)]
+    grad_ts = [38] * B
+    cs = {"mixed": [0.0, 3e38, 60.0, 5.0, 0.0, 400.0], "all_every_push": [0.0] * B,
+          "truncated": [20.0] * B, "nothing": [3e38] * B}[case]
+    cap = 9_999 if case == "truncated" else P
+    idx, val, cnt, seg = _lists_from_singles(a, grads, cs, Ts, clients, cap, dev)
+    torch.cuda.synchronize()
+    counts = cnt.cpu().numpy()
+    if case == "truncated":
+        assert (counts > cap).all()
+    if case == "nothing":
+        assert (counts == 0).all()
+    for k in range(B):
+        fa.bfasgd_apply_sparse(a, idx[k], val[k], cnt[k:k + 1], clients[k], grad_ts[k])
+    fa.fasgd_apply_pushes(b, idx, val, cnt, seg, clients, grad_ts)
+    _assert_same(a, b)
+
+
+def test_apply_pushes_matches_oracle():
+    """Against the oracle: B pushes selected from the batch's v, then applied
+    one by one at T, T + 1, ..."""
+    import torch
+    dev = gpu()
+    P, B = 300_007, 12
+    (st,), ref, (m_, s_, w), keep = _mid_run_state(P, dev, seed=12, copies=1)
+    grads_h = [workload.host_gradient(w, m_, s_, 100 + k, seed=12) for k in range(B)]
+    Ts, clients = [40 + k for k in range(B)], [k % w.lam for k in range(B)]
+    grad_ts = [max(40 + k - 3, 0) for k in range(B)]
+    idx, val, cnt, seg, ws = _batch_buffers(B, P, P, dev)
+    fa.bfasgd_select_compact_batch(st, [to_dev(g, dev) for g in grads_h], 60.0, 1e-8, SEED, Ts, clients,
+                                   idx, val, cnt, ws, seg_start=seg)
+    fa.fasgd_apply_pushes(st, idx, val, cnt, seg, clients, grad_ts)
+    v32 = ref.v.astype(np.float32)
+    lists = [oracle.bfasgd_select(v32, grads_h[k], 60.0, 1e-8, SEED, Ts[k], clients[k]) for k in range(B)]
+    for k, (r_idx, r_val, r_m) in enumerate(lists):
+        oracle.bfasgd_apply_sparse(ref, r_idx, r_val, grad_ts[k])
+    torch.cuda.synchronize()
+    assert [int(x) for x in cnt.cpu()] == [r[2] for r in lists]
+    assert_state_close(st, ref, RTOL_SEQ, what=f"{B} pushes in one pass")
+    assert st.T == ref.T == 40 + B
