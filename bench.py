@@ -1,17 +1,20 @@
 """Benchmark of the FASGD parameter-server step on one MI355X.
 
 One step = the whole server path over one batch of client gradients:
-  1. fasgd_apply_updates  K gradients fused in one pass (dense FASGD,
-                          eqs. of Sec. 2.2, K-fold state reuse);
-  2. bfasgd_select_compact one more client's push, per-parameter send/skip
-                          (Sec. 2.3) and compaction into (index, value);
-  3. bfasgd_apply_sparse  the server applies that compacted push.
+  1. fasgd_apply_with_push  one pass that applies the B-FASGD push selected
+                            in the previous step (Sec. 2.3) and then K client
+                            gradients (dense FASGD, eqs. of Sec. 2.2, K-fold
+                            state reuse);
+  2. bfasgd_select_compact  the next client's push: per-parameter send/skip
+                            and compaction into (index, value) lists.
 Inputs (state and a pool of K + 1 distinct synthetic gradients) are resident
 in HBM before timing; every step uses fresh (client, timestamp) pairs.
 
 Prints ONE JSON line.  value = parameter updates applied per second
-(P*K dense + m sparse per step).  roofline = the dense apply kernel's
-algorithmic HBM bytes per launch over its average event-timed duration.
+(P*K dense + m sparse per step).  roofline = the fused pass's algorithmic
+HBM bytes per launch over its average event-timed duration.  Further legs,
+timed after the step, cover the other entry points, and B-FASGD pushes
+handled one by one or in batches at the 784-1000-1000-10 MLP's size.
 """
 import argparse
 import hashlib
@@ -92,6 +95,82 @@ def cpu_baseline(pool, theta0_host, clients, ts, c, w, K, P_s):
     oracle.bfasgd_apply_sparse(st, idx, val, ts[K])
     dt = time.perf_counter() - t0
     return (P_s * K + m) / dt, dt, m
+
+
+def mlp_push_batches(fa, workload, dev, mode, B=16, reps=20):
+    """B-FASGD at the MLP's size (1.8M parameters, lambda = 16, about 20 %
+    transmitted): B pushes handled one by one (a selection, then a sparse
+    apply, per push) or in one batch (bfasgd_select_compact_batch, then
+    fasgd_apply_pushes).  Both give the same state; per-batch times are for
+    `reps` batches back to back."""
+    import numpy as np
+    import torch
+    w = workload.WORKLOADS["mlp_bfasgd"]
+    P = w.P
+    theta0, m_, s_ = workload.host_params(w)
+    grads = [torch.from_numpy(workload.host_gradient(w, m_, s_, t)).to(dev) for t in range(B)]
+    theta, n, b, v, last_T = fa.allocate_state(P, dev)
+    theta.copy_(torch.from_numpy(theta0))
+    st = fa.fasgd_init_state(theta, n, b, v, last_T, lam=w.lam, alpha=w.alpha_fasgd, math_mode=mode)
+    clients, ts = workload.schedule(w, B + 4 * (reps + 2) * B)
+    fa.fasgd_apply_updates(st, grads, clients[:B], ts[:B])     # gives v its scale
+    torch.cuda.synchronize()
+    c = calibrate_c(v, w.transmit_fraction or 0.2)
+    L = fa.bfasgd_list_index_length(P)
+    idx = torch.empty((B, P), device=dev, dtype=torch.int32)
+    val = torch.empty((B, P), device=dev)
+    cnt = torch.zeros(B, device=dev, dtype=torch.int64)
+    seg = torch.empty((B, L), device=dev, dtype=torch.int32)
+    ws = torch.empty(B * fa.bfasgd_workspace_bytes(P), device=dev, dtype=torch.uint8)
+    ws1 = fa.allocate_workspace(P, dev)
+
+    def one_by_one():
+        for k in range(B):
+            T = st.T
+            fa.bfasgd_select_compact(st, grads[k], c, EPS_C, SEED, T, clients[T], idx[k], val[k],
+                                     cnt[k:k + 1], ws1)
+            fa.bfasgd_apply_sparse(st, idx[k], val[k], cnt[k:k + 1], clients[T], ts[T])
+
+    def batched_select():
+        T = st.T
+        fa.bfasgd_select_compact_batch(st, grads, c, EPS_C, SEED, list(range(T, T + B)), clients[T:T + B],
+                                       idx, val, cnt, ws, seg_start=seg)
+
+    def batched_apply():
+        T = st.T
+        fa.fasgd_apply_pushes(st, idx, val, cnt, seg, clients[T:T + B], ts[T:T + B])
+
+    def batched():
+        batched_select()
+        batched_apply()
+
+    def per_batch_ms(fn):
+        fn()
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(e) / reps
+
+    seq_ms = per_batch_ms(one_by_one)
+    bat_ms = per_batch_ms(batched)
+    sel_ms = per_batch_ms(batched_select)
+    m_avg = float(cnt.double().mean().item())
+    app_ms = per_batch_ms(batched_apply)
+    # algorithmic bytes: each selection reads v and g and writes (idx, val)
+    # and its list index; the batched apply reads and writes the state once
+    # (plus last_T of the listed parameters) and reads every list
+    sel_bytes = B * (8 * P + 8 * m_avg + 4 * L)
+    touched = P * (1.0 - (1.0 - m_avg / P) ** B)
+    app_bytes = 32 * P + 4 * touched + B * (8 * m_avg + 8 * L)
+    return {"P": P, "B": B, "lambda": w.lam, "c": c, "transmitted_fraction": m_avg / P,
+            "ms_per_batch_one_by_one": seq_ms, "ms_per_batch_batched": bat_ms,
+            "speedup": seq_ms / bat_ms,
+            "param_updates_per_s_batched": B * m_avg / (bat_ms * 1e-3),
+            "bfasgd_select_compact_batch": {"ms": sel_ms, "GB/s": sel_bytes / (sel_ms * 1e-3) / 1e9},
+            "fasgd_apply_pushes": {"ms": app_ms, "GB/s": app_bytes / (app_ms * 1e-3) / 1e9}}
 
 
 def main():
@@ -338,6 +417,7 @@ def main():
         cp_ms.append(a.elapsed_time(b_))
     copy_gbs = 8 * P / (float(np.mean(cp_ms[1:])) * 1e-3) / 1e9
     del anchor
+    batches = mlp_push_batches(fa, workload, dev, mode)
 
     out = {
         "metric": METRIC,
@@ -385,6 +465,7 @@ def main():
             "bfasgd_apply_segments": {"ms_all_sent": segapply_ms,
                                       "GB/s": 40 * P / (segapply_ms * 1e-3) / 1e9},
             "copy_anchor": {"GB/s": copy_gbs, "bytes": 8 * P},
+            "push_batches_mlp": batches,
         },
     }
     if args.cpu_params:

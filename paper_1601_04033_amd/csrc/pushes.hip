@@ -8,10 +8,13 @@
 // Each list is one that the selection wrote with its list index, so the
 // entries of push b for the 256-parameter segment s are at [seg_start_b[s],
 // seg_start_b[s + 1]) of its list, clipped to min(count_b, capacity).  One
-// wave owns one segment (64 lanes x 4 parameters); lane b of the wave first
-// finds push b's range, then the wave loads the first 64 entries of
-// kGroup pushes at once and applies them one push at a time through an LDS
-// slice holding one value and one flag byte per parameter.
+// wave owns one segment (64 lanes x 4 parameters): lane b of the wave first
+// finds push b's range; the wave loads its segment's state into LDS and the
+// first 64 entries of kGroup pushes at once, and applies the pushes one at
+// a time, each lane updating the LDS state of the parameter its entry
+// names.  A push thus costs one update per listed parameter (a lane-owns-
+// parameters layout would evaluate the update for all four parameters of
+// every lane in every push, and be bound by the vector ALU).
 //
 // Traffic: the state is read and written once (16 + 16 bytes per parameter,
 // plus 4 bytes of last_T per parameter that some push lists) and every list
@@ -29,6 +32,7 @@ constexpr int kBlock = 128;
 constexpr int kWave = 64;
 constexpr int kWavesPerBlock = kBlock / kWave;
 constexpr int kGroup = 8;   // pushes whose entries are loaded together
+constexpr int kEntries = 1; // entries per lane of each push loaded ahead (64 each)
 static_assert(kWave * 4 == kPushSeg, "one wave covers one list-index segment");
 static_assert(kMaxBatch <= kWave, "lane b holds the range of push b");
 
@@ -83,13 +87,37 @@ __device__ __forceinline__ void stage_entry(int32_t j, float x, int64_t first, i
     }
 }
 
-// Thread i of the vector kernel owns parameters 4i .. 4i+3; the thread after
-// the last full chunk owns the P mod 4 tail.
+// The wave's 256 parameters: theta, n, b, v and the last push that listed
+// each one, in LDS for the whole pass.
+struct SegState {
+    float x[4][kPushSeg];
+    int last[kPushSeg];
+};
+
+// Apply list entry (j, g) of push pb to the LDS copy of the state, when j
+// lies in this wave's segment and below P.
+template <int MODE>
+__device__ __forceinline__ void apply_entry(SegState& s, int32_t j, float g, int pb, float coef, int64_t first,
+                                            int64_t P, const Hyper& h)
+{
+    const int64_t r = static_cast<int64_t>(j) - first;
+    if (j >= 0 && r >= 0 && r < kPushSeg && first + r < P) {
+        float t = s.x[0][r], nn = s.x[1][r], bb = s.x[2][r], vv = s.x[3][r];
+        fasgd_step<MODE>(t, nn, bb, vv, g, coef, h);
+        s.x[0][r] = t; s.x[1][r] = nn; s.x[2][r] = bb; s.x[3][r] = vv;
+        s.last[r] = pb;
+    }
+}
+
+// Thread i of the vector kernel loads and stores parameters 4i .. 4i+3 (the
+// thread after the last full chunk the P mod 4 tail); in between, the state
+// of the wave's segment lives in LDS and each push's entries are applied
+// there, one entry per lane, so a push costs one update per listed
+// parameter rather than one per parameter.
 template <int MODE>
 __global__ __launch_bounds__(kBlock) void apply_pushes_vec(const PushBatchArgs a)
 {
-    __shared__ float s_val[kWavesPerBlock][kPushSeg];
-    __shared__ uint32_t s_flag[kWavesPerBlock][kWave];   // byte c of word l: parameter 4 l + c listed
+    __shared__ SegState s_seg[kWavesPerBlock];
     const Hyper h = a.h;
     const int B = a.B;
     const int64_t nvec = a.P >> 2;
@@ -99,6 +127,7 @@ __global__ __launch_bounds__(kBlock) void apply_pushes_vec(const PushBatchArgs a
     const int64_t seg = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + w;
     const int64_t first = seg * kPushSeg;
     const int64_t o = i * 4;
+    SegState& S = s_seg[w];
     uint32_t lo, hi;
     lane_range(a, seg, lane, lo, hi);
     if (__builtin_amdgcn_ballot_w64(hi > lo) == 0) return;   // no push lists a parameter of this segment
@@ -109,24 +138,31 @@ __global__ __launch_bounds__(kBlock) void apply_pushes_vec(const PushBatchArgs a
     } else {
         for (int c = 0; c < valid; ++c) { th[c] = a.theta[o + c]; n[c] = a.n[o + c]; b[c] = a.b[o + c]; v[c] = a.v[o + c]; }
     }
-    int last[4] = {-1, -1, -1, -1};
-    uint8_t* flag_bytes = reinterpret_cast<uint8_t*>(s_flag[w]);
     for (int g0 = 0; g0 < B; g0 += kGroup) {
-        int32_t e_idx[kGroup];
-        float e_val[kGroup];
+        int32_t e_idx[kGroup][kEntries];
+        float e_val[kGroup][kEntries];
 #pragma unroll
         for (int u = 0; u < kGroup; ++u) {
-            e_idx[u] = -1;
-            e_val[u] = 0.0f;
             const int pb = g0 + u;
-            if (pb < B) {
-                const uint32_t l = __builtin_amdgcn_readlane(lo, pb), e = __builtin_amdgcn_readlane(hi, pb);
-                if (l + lane < e) {
-                    const int64_t at = static_cast<int64_t>(pb) * a.list_stride + l + lane;
-                    e_idx[u] = a.idx[at];
-                    e_val[u] = a.val[at];
+            const uint32_t l = pb < B ? __builtin_amdgcn_readlane(lo, pb) : 0u;
+            const uint32_t e = pb < B ? __builtin_amdgcn_readlane(hi, pb) : 0u;
+#pragma unroll
+            for (int q = 0; q < kEntries; ++q) {
+                e_idx[u][q] = -1;
+                e_val[u][q] = 0.0f;
+                if (l + q * kWave + lane < e) {
+                    const int64_t at = static_cast<int64_t>(pb) * a.list_stride + l + q * kWave + lane;
+                    e_idx[u][q] = a.idx[at];
+                    e_val[u][q] = a.val[at];
                 }
             }
+        }
+        if (g0 == 0) {   // the state, once its loads (issued before the entries') are in
+            *reinterpret_cast<f4*>(&S.x[0][4 * lane]) = th;
+            *reinterpret_cast<f4*>(&S.x[1][4 * lane]) = n;
+            *reinterpret_cast<f4*>(&S.x[2][4 * lane]) = b;
+            *reinterpret_cast<f4*>(&S.x[3][4 * lane]) = v;
+            *reinterpret_cast<i4*>(&S.last[4 * lane]) = i4{-1, -1, -1, -1};
         }
 #pragma unroll
         for (int u = 0; u < kGroup; ++u) {
@@ -134,32 +170,26 @@ __global__ __launch_bounds__(kBlock) void apply_pushes_vec(const PushBatchArgs a
             if (pb >= B) break;
             const uint32_t l = __builtin_amdgcn_readlane(lo, pb), e = __builtin_amdgcn_readlane(hi, pb);
             if (l == e) continue;   // push pb lists nothing here
+            const float coef = a.coef[pb];
+            // the entries of one push are distinct parameters; the previous
+            // push's updates are in LDS before this push reads them
             wave_lds_order();
-            s_flag[w][lane] = 0u;
-            wave_lds_order();
-            stage_entry(e_idx[u], e_val[u], first, kPushSeg, a.P, s_val[w], flag_bytes);
-            if (e - l > static_cast<uint32_t>(kWave)) {   // more than 64 entries in 256 parameters
-                const int64_t base = static_cast<int64_t>(pb) * a.list_stride;
-                for (uint32_t x = l + kWave + lane; x < e; x += kWave)
-                    stage_entry(a.idx[base + x], a.val[base + x], first, kPushSeg, a.P, s_val[w], flag_bytes);
-            }
-            wave_lds_order();
-            const uint32_t flags = s_flag[w][lane];
-            if (flags) {
-                const f4 pv = *reinterpret_cast<const f4*>(&s_val[w][4 * lane]);
-                const float coef = a.coef[pb];
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    if ((flags >> (8 * c)) & 0xffu) {
-                        float t = th[c], nn = n[c], bb = b[c], vv = v[c];
-                        fasgd_step<MODE>(t, nn, bb, vv, pv[c], coef, h);
-                        th[c] = t; n[c] = nn; b[c] = bb; v[c] = vv;
-                        last[c] = pb;
-                    }
-                }
+            for (int q = 0; q < kEntries; ++q)
+                apply_entry<MODE>(S, e_idx[u][q], e_val[u][q], pb, coef, first, a.P, h);
+            if (e - l > static_cast<uint32_t>(kEntries * kWave)) {   // more entries than were loaded ahead
+                const int64_t base = static_cast<int64_t>(pb) * a.list_stride;
+                for (uint32_t x = l + kEntries * kWave + lane; x < e; x += kWave)
+                    apply_entry<MODE>(S, a.idx[base + x], a.val[base + x], pb, coef, first, a.P, h);
             }
         }
     }
+    wave_lds_order();
+    th = *reinterpret_cast<const f4*>(&S.x[0][4 * lane]);
+    n = *reinterpret_cast<const f4*>(&S.x[1][4 * lane]);
+    b = *reinterpret_cast<const f4*>(&S.x[2][4 * lane]);
+    v = *reinterpret_cast<const f4*>(&S.x[3][4 * lane]);
+    const i4 last = *reinterpret_cast<const i4*>(&S.last[4 * lane]);
     if (valid == 4) {
         st4(a.theta + o, th); st4(a.n + o, n); st4(a.b + o, b); st4(a.v + o, v);
         if ((last[0] | last[1] | last[2] | last[3]) >= 0) {   // all four listed
