@@ -13,8 +13,9 @@ in HBM before timing; every step uses fresh (client, timestamp) pairs.
 Prints ONE JSON line.  value = parameter updates applied per second
 (P*K dense + m sparse per step).  roofline = the fused pass's algorithmic
 HBM bytes per launch over its average event-timed duration.  Further legs,
-timed after the step, cover the other entry points, and B-FASGD pushes
-handled one by one or in batches at the 784-1000-1000-10 MLP's size.
+timed after the step, cover the other entry points and the small workloads
+(100k parameters; the 784-1000-1000-10 MLP's 1.8M, with B-FASGD pushes
+handled one by one or in batches), eagerly and as replayed HIP graphs.
 """
 import argparse
 import hashlib
@@ -97,25 +98,93 @@ def cpu_baseline(pool, theta0_host, clients, ts, c, w, K, P_s):
     return (P_s * K + m) / dt, dt, m
 
 
-def mlp_push_batches(fa, workload, dev, mode, B=16, reps=20):
-    """B-FASGD at the MLP's size (1.8M parameters, lambda = 16, about 20 %
-    transmitted): B pushes handled one by one (a selection, then a sparse
-    apply, per push) or in one batch (bfasgd_select_compact_batch, then
-    fasgd_apply_pushes).  Both give the same state; per-batch times are for
-    `reps` batches back to back."""
-    import numpy as np
+def small_configs(fa, workload, dev, mode, B=16, reps=20):
+    """The small workloads, whose state fits the 256 MB Infinity Cache (so
+    their GB/s are 'effective', not HBM): the tiny trace (100k parameters,
+    K = 1, FASGD and SASGD), the MLP-shaped FASGD pass (1.8M parameters,
+    K = 16) and MLP-sized B-FASGD (about 20 % per push), with B pushes handled
+    one by one (a selection and a sparse apply each) or batched
+    (bfasgd_select_compact_batch, then fasgd_apply_pushes; the same state).
+    Each operation is timed over `reps` calls issued back to back by the host
+    and over the same calls captured in one HIP graph and replayed, which
+    takes the host's per-call work and most launch gaps out."""
     import torch
+
+    def eager_ms(fn):
+        fn()
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(e) / reps
+
+    def graph_ms(fn):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        g.replay()
+        e.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(e) / reps
+
+    def measure(fn, nbytes, updates):
+        ea, gr = eager_ms(fn), graph_ms(fn)
+        return {"us_eager": ea * 1e3, "us_graph": gr * 1e3, "GB/s_effective": nbytes / (gr * 1e-3) / 1e9,
+                "param_updates_per_s": updates / (gr * 1e-3)}
+
+    def new_state(w, sasgd=False):
+        theta0, m_, s_ = workload.host_params(w)
+        theta, n, b, v, last_T = fa.allocate_state(w.P, dev, with_stats=not sasgd)
+        theta.copy_(torch.from_numpy(theta0))
+        st = fa.fasgd_init_state(theta, n, b, v, last_T, lam=w.lam,
+                                 alpha=w.alpha_sasgd if sasgd else w.alpha_fasgd, math_mode=mode)
+        return st, m_, s_
+
+    out = {}
+    # tiny trace: K = 1 passes
+    w = workload.WORKLOADS["tiny"]
+    n_calls = 2 * reps + 4
+    for name, sasgd in (("tiny_fasgd_k1", False), ("tiny_sasgd_k1", True)):
+        st, m_, s_ = new_state(w, sasgd)
+        g1 = torch.from_numpy(workload.host_gradient(w, m_, s_, 0)).to(dev)
+        clients, ts = workload.schedule(w, n_calls)
+        call = fa.sasgd_apply_updates if sasgd else fa.fasgd_apply_updates
+
+        def one(st=st, g1=g1, clients=clients, ts=ts, call=call):
+            T = st.T
+            call(st, [g1], clients[T:T + 1], ts[T:T + 1])
+        out[name] = measure(one, w.P * (12 if sasgd else 36), w.P)
+        out[name]["P"] = w.P
+
+    # MLP-shaped FASGD: K = 16 gradients per pass
+    w = workload.WORKLOADS["mlp"]
+    K = 16
+    st, m_, s_ = new_state(w)
+    grads = [torch.from_numpy(workload.host_gradient(w, m_, s_, t)).to(dev) for t in range(K)]
+    clients, ts = workload.schedule(w, K * (2 * reps + 4))
+
+    def mlp_pass():
+        T = st.T
+        fa.fasgd_apply_updates(st, grads, clients[T:T + K], ts[T:T + K])
+    out["mlp_fasgd_k16"] = measure(mlp_pass, w.P * (32 + 4 * K), w.P * K)
+    out["mlp_fasgd_k16"].update({"P": w.P, "K": K})
+
+    # MLP-sized B-FASGD: B pushes one by one or batched
     w = workload.WORKLOADS["mlp_bfasgd"]
     P = w.P
-    theta0, m_, s_ = workload.host_params(w)
+    st, m_, s_ = new_state(w)
     grads = [torch.from_numpy(workload.host_gradient(w, m_, s_, t)).to(dev) for t in range(B)]
-    theta, n, b, v, last_T = fa.allocate_state(P, dev)
-    theta.copy_(torch.from_numpy(theta0))
-    st = fa.fasgd_init_state(theta, n, b, v, last_T, lam=w.lam, alpha=w.alpha_fasgd, math_mode=mode)
-    clients, ts = workload.schedule(w, B + 4 * (reps + 2) * B)
+    clients, ts = workload.schedule(w, B + 8 * (reps + 2) * B)
     fa.fasgd_apply_updates(st, grads, clients[:B], ts[:B])     # gives v its scale
     torch.cuda.synchronize()
-    c = calibrate_c(v, w.transmit_fraction or 0.2)
+    c = calibrate_c(st.v, w.transmit_fraction or 0.2)
     L = fa.bfasgd_list_index_length(P)
     idx = torch.empty((B, P), device=dev, dtype=torch.int32)
     val = torch.empty((B, P), device=dev)
@@ -144,33 +213,30 @@ def mlp_push_batches(fa, workload, dev, mode, B=16, reps=20):
         batched_select()
         batched_apply()
 
-    def per_batch_ms(fn):
-        fn()
-        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        for _ in range(reps):
-            fn()
-        e.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(e) / reps
-
-    seq_ms = per_batch_ms(one_by_one)
-    bat_ms = per_batch_ms(batched)
-    sel_ms = per_batch_ms(batched_select)
+    seq = measure(one_by_one, 0, 0)
+    bat = measure(batched, 0, 0)
+    sel = measure(batched_select, 0, 0)
     m_avg = float(cnt.double().mean().item())
-    app_ms = per_batch_ms(batched_apply)
+    app = measure(batched_apply, 0, 0)
     # algorithmic bytes: each selection reads v and g and writes (idx, val)
     # and its list index; the batched apply reads and writes the state once
     # (plus last_T of the listed parameters) and reads every list
     sel_bytes = B * (8 * P + 8 * m_avg + 4 * L)
     touched = P * (1.0 - (1.0 - m_avg / P) ** B)
     app_bytes = 32 * P + 4 * touched + B * (8 * m_avg + 8 * L)
-    return {"P": P, "B": B, "lambda": w.lam, "c": c, "transmitted_fraction": m_avg / P,
-            "ms_per_batch_one_by_one": seq_ms, "ms_per_batch_batched": bat_ms,
-            "speedup": seq_ms / bat_ms,
-            "param_updates_per_s_batched": B * m_avg / (bat_ms * 1e-3),
-            "bfasgd_select_compact_batch": {"ms": sel_ms, "GB/s": sel_bytes / (sel_ms * 1e-3) / 1e9},
-            "fasgd_apply_pushes": {"ms": app_ms, "GB/s": app_bytes / (app_ms * 1e-3) / 1e9}}
+    for d, nb in ((sel, sel_bytes), (app, app_bytes)):
+        d["GB/s_effective"] = nb / (d["us_graph"] * 1e-6) / 1e9
+    for d in (seq, bat):
+        d.pop("GB/s_effective")
+        d["param_updates_per_s"] = B * m_avg / (d["us_graph"] * 1e-6)
+    for d in (sel, app):
+        d.pop("param_updates_per_s")
+    out["mlp_bfasgd_pushes"] = {
+        "P": P, "B": B, "lambda": w.lam, "c": c, "transmitted_fraction": m_avg / P,
+        "one_by_one": seq, "batched": bat,
+        "speedup_eager": seq["us_eager"] / bat["us_eager"], "speedup_graph": seq["us_graph"] / bat["us_graph"],
+        "bfasgd_select_compact_batch": sel, "fasgd_apply_pushes": app}
+    return out
 
 
 def main():
@@ -417,7 +483,7 @@ def main():
         cp_ms.append(a.elapsed_time(b_))
     copy_gbs = 8 * P / (float(np.mean(cp_ms[1:])) * 1e-3) / 1e9
     del anchor
-    batches = mlp_push_batches(fa, workload, dev, mode)
+    small = small_configs(fa, workload, dev, mode)
 
     out = {
         "metric": METRIC,
@@ -465,7 +531,7 @@ def main():
             "bfasgd_apply_segments": {"ms_all_sent": segapply_ms,
                                       "GB/s": 40 * P / (segapply_ms * 1e-3) / 1e9},
             "copy_anchor": {"GB/s": copy_gbs, "bytes": 8 * P},
-            "push_batches_mlp": batches,
+            "small_configs": small,
         },
     }
     if args.cpu_params:
