@@ -71,3 +71,16 @@ def sample_indices(P, k=4096, seed=0):
     js = np.concatenate([np.arange(min(64, P)), np.arange(max(P - 64, 0), P),
                          rng.integers(0, P, size=k)])
     return np.unique(js)
+
+
+def philox_r(js, seed, T, client):
+    """r_j of the oracle's Philox stream for the given indices."""
+    import oracle
+    out = np.empty(len(js))
+    for i, j in enumerate(js):
+        j = int(j)
+        q = j >> 2
+        w = oracle.philox4x32_10([q & 0xFFFFFFFF, q >> 32, T & 0xFFFFFFFF, client],
+                                 [seed & 0xFFFFFFFF, seed >> 32])[j & 3]
+        out[i] = (int(w) >> 8) * 2.0 ** -24
+    return out

@@ -10,7 +10,7 @@ import pytest
 import oracle
 import paper_1601_04033_amd as fa
 import workload
-from helpers import RTOL_SEQ, assert_state_close, gpu, to_dev
+from helpers import RTOL_SEQ, assert_state_close, gpu, new_gpu_state, philox_r, sample_indices, to_dev
 
 pytestmark = pytest.mark.gpu
 SEED = 0xBA7C4
@@ -221,3 +221,79 @@ def test_apply_pushes_matches_oracle():
     assert [int(x) for x in cnt.cpu()] == [r[2] for r in lists]
     assert_state_close(st, ref, RTOL_SEQ, what=f"{B} pushes in one pass")
     assert st.T == ref.T == 40 + B
+
+
+def test_mlp_bfasgd_batched_sequence_sampled():
+    """MLP layout, lambda = 16: one dense pass of 16 updates, then 2,000
+    pushes at about 20 % in 125 batches of 16, each batch selected from v at
+    the batch's start and applied in one pass.  The oracle follows a sample of
+    parameters, decides every push of a batch from its own v at that point
+    and applies the pushes one by one.  A decision may differ only where the
+    oracle's threshold lies within v's tolerance of r; such indices are
+    dropped from later comparisons."""
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["mlp_bfasgd"]
+    P, U, W, B = w.P, 2000, 16, 16
+    theta0, m_, s_ = workload.host_params(w)
+    clients, ts = workload.schedule(w, U + W)
+    dm, ds = to_dev(m_, dev), to_dev(s_, dev)
+    st = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, fa.MATH_FAST)
+    js = sample_indices(P, 3000, seed=7)
+    jt = torch.from_numpy(js).to(dev)
+    ref = oracle.init_state(theta0[js], alpha=w.alpha_fasgd)
+    gb = [torch.empty(P, device=dev) for _ in range(B)]
+    for k in range(W):
+        workload.device_gradient(w, dm, ds, k, out=gb[k])
+    fa.fasgd_apply_updates(st, gb[:W], clients[:W], ts[:W])
+    for k in range(W):
+        oracle.fasgd_apply(ref, gb[k][jt].cpu().numpy(), ts[k])
+    vd = ref.v + 1e-8
+    lo, hi = 0.0, 1e6
+    for _ in range(80):
+        c = 0.5 * (lo + hi)
+        lo, hi = (c, hi) if (vd / (vd + c)).mean() > 0.2 else (lo, c)
+    c = oracle.f32(c)
+    idx, val, cnt, seg, ws = _batch_buffers(B, P, P, dev)
+    mask = torch.zeros(P, device=dev, dtype=torch.bool)
+    alive = np.ones(js.size, bool)
+    flips = 0
+    fractions = []
+    for t0 in range(W, W + U, B):
+        for k in range(B):
+            workload.device_gradient(w, dm, ds, t0 + k, out=gb[k])
+        T0 = st.T
+        assert T0 == ref.T == t0
+        fa.bfasgd_select_compact_batch(st, gb, c, 1e-8, SEED, list(range(T0, T0 + B)), clients[t0:t0 + B],
+                                       idx, val, cnt, ws, seg_start=seg)
+        v32 = ref.v.astype(np.float32)           # every push of the batch decides from this v
+        counts = cnt.cpu().numpy()
+        wants = []
+        for k in range(B):
+            m = int(counts[k])
+            fractions.append(m / P)
+            mask.zero_()
+            mask[idx[k, :m].long()] = True
+            got = mask[jt].cpu().numpy()
+            want = oracle.bfasgd_decide(js, v32, c, 1e-8, SEED, T0 + k, clients[t0 + k])
+            diff = alive & (got != want)
+            if diff.any():
+                tv = v32[diff].astype(np.float64) + 1e-8
+                p = tv / (tv + c)
+                r = philox_r(js[diff], SEED, T0 + k, int(clients[t0 + k]))
+                assert (np.abs(r - p) <= 2 * RTOL_SEQ * p).all(), (r, p)
+                flips += int(diff.sum())
+                alive &= ~diff
+            wants.append(want)
+        g_at = [g[jt].cpu().numpy() for g in gb]
+        for k in range(B):
+            sel = np.flatnonzero(wants[k] & alive)
+            oracle.bfasgd_apply_sparse(ref, sel.astype(np.int32), g_at[k][sel], ts[t0 + k])
+        fa.fasgd_apply_pushes(st, idx, val, cnt, seg, clients[t0:t0 + B], ts[t0:t0 + B])
+    torch.cuda.synchronize()
+    assert flips <= js.size // 100, flips
+    keep = np.flatnonzero(alive)
+    assert_state_close(st, ref.take(keep), RTOL_SEQ, js=torch.from_numpy(js[keep]).to(dev),
+                       what="after 2000 pushes in batches of 16")
+    assert 0.15 < np.mean(fractions) < 0.35, np.mean(fractions)
+

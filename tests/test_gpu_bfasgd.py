@@ -11,7 +11,8 @@ import pytest
 import oracle
 import paper_1601_04033_amd as fa
 import workload
-from helpers import RTOL_ONE, RTOL_SEQ, assert_close, assert_state_close, gpu, new_gpu_state, sample_indices, to_dev
+from helpers import (RTOL_ONE, RTOL_SEQ, assert_close, assert_state_close, gpu, new_gpu_state, philox_r,
+                     sample_indices, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -186,18 +187,6 @@ def test_partial_push_matches_oracle(mode):
     np.testing.assert_array_equal(st.v.cpu().numpy()[rest], v0[rest])
 
 
-def _philox_r(js, seed, T, client):
-    """r_j of the oracle's Philox stream for the given indices."""
-    out = np.empty(len(js))
-    for i, j in enumerate(js):
-        j = int(j)
-        q = j >> 2
-        w = oracle.philox4x32_10([q & 0xFFFFFFFF, q >> 32, T & 0xFFFFFFFF, client],
-                                 [seed & 0xFFFFFFFF, seed >> 32])[j & 3]
-        out[i] = (int(w) >> 8) * 2.0 ** -24
-    return out
-
-
 def test_mlp_bfasgd_sequence_sampled():
     """MLP layout, lambda = 16: one dense pass of 16 updates (v starts at 0,
     and v = 0 would never transmit), then 2,000 pushes each selected at about
@@ -253,7 +242,7 @@ def test_mlp_bfasgd_sequence_sampled():
         if diff.any():
             tv = v32[diff].astype(np.float64) + 1e-8
             p = tv / (tv + c)
-            r = _philox_r(js[diff], SEED, ref.T, int(clients[t]))
+            r = philox_r(js[diff], SEED, ref.T, int(clients[t]))
             assert (np.abs(r - p) <= 2 * RTOL_SEQ * p).all(), (r, p)
             flips += int(diff.sum())
             alive &= ~diff

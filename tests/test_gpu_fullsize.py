@@ -8,7 +8,7 @@ import pytest
 import oracle
 import paper_1601_04033_amd as fa
 import workload
-from helpers import RTOL_SEQ, assert_close, assert_state_close, gpu, new_gpu_state, sample_indices
+from helpers import RTOL_SEQ, assert_close, assert_state_close, gpu, new_gpu_state, philox_r, sample_indices
 
 pytestmark = pytest.mark.gpu
 SEED = 0x5EED
@@ -28,17 +28,6 @@ def _calibrate_c(v, target):
         c = 0.5 * (lo + hi)
         lo, hi = (c, hi) if (vd / (vd + c)).mean() > target else (lo, c)
     return oracle.f32(c)
-
-
-def _philox_r(js, seed, T, client):
-    out = np.empty(len(js))
-    for i, j in enumerate(js):
-        j = int(j)
-        q = j >> 2
-        w = oracle.philox4x32_10([q & 0xFFFFFFFF, q >> 32, T & 0xFFFFFFFF, client],
-                                 [seed & 0xFFFFFFFF, seed >> 32])[j & 3]
-        out[i] = (int(w) >> 8) * 2.0 ** -24
-    return out
 
 
 def test_memscale_1e9_step_sampled():
@@ -87,7 +76,7 @@ def test_memscale_1e9_step_sampled():
     if diff.any():     # only near-ties of the fp32 v drift may differ
         tv = v32[diff].astype(np.float64) + 1e-8
         p = tv / (tv + c)
-        assert (np.abs(_philox_r(js[diff], SEED, ref.T, int(clients[K])) - p) <= 2 * RTOL_SEQ * p).all()
+        assert (np.abs(philox_r(js[diff], SEED, ref.T, int(clients[K])) - p) <= 2 * RTOL_SEQ * p).all()
         assert diff.sum() <= 4
     g_at = gK[jt].cpu().numpy()
     sel = np.flatnonzero(want & ~diff)
@@ -154,7 +143,7 @@ def test_memscale_1e9_fused_step_sampled():
     if diff.any():
         tv = v32[diff].astype(np.float64) + 1e-8
         p = tv / (tv + c)
-        assert (np.abs(_philox_r(js[diff], SEED, ref.T, int(clients[K])) - p) <= 2 * RTOL_SEQ * p).all()
+        assert (np.abs(philox_r(js[diff], SEED, ref.T, int(clients[K])) - p) <= 2 * RTOL_SEQ * p).all()
         assert diff.sum() <= 4
     sel = np.flatnonzero(want & ~diff)
     sl = slice(K + 1, 2 * K + 1)
