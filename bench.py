@@ -288,50 +288,63 @@ def main():
     seg = torch.empty(fa.bfasgd_list_index_length(P), device=dev, dtype=torch.int32)
     per_step = K + 1
     # timestamps used: K (first pass) + (K + 1) per step + 1 (the last push),
-    # then the legs after the timed region: 3 steps of separate calls, 3
-    # SASGD passes of K, 3 cached pushes, 3 segment pushes, 3 synchronous
-    # steps and the dense passes at K = 1, 8, 32 (11 calls each)
+    # then the legs after the timed region: 3 steps of separate calls, 3 of
+    # two calls (+ 1 push), 3 SASGD passes of K, 3 cached pushes, 3 segment
+    # pushes, 3 synchronous steps and the dense passes at K = 1, 8, 32 (11
+    # calls each)
     KS = (1, 8, 32)
-    clients, ts = workload.schedule(w, K + (warm + steps + 3) * per_step + 1 + 3 * K + 9 + 16 + 11 * sum(KS))
+    clients, ts = workload.schedule(w, K + (warm + steps + 6) * per_step + 2 + 3 * K + 9 + 16 + 11 * sum(KS))
     torch.cuda.synchronize()
 
-    # One step: a single pass that applies the push selected in the previous
-    # step (at its timestamp T) and then K client gradients (T + 1 ... T + K),
-    # then the selection of this step's push (applied at T + K + 1 by the
-    # next pass).  That is the order in which the server lock serialises the
-    # arrivals, and per step the work is K dense updates, one push selected
-    # and one push applied.  The first step of the warm-up has no push to
-    # apply; the push selected by the last timed step is applied after the
-    # timed region.
+    # One step: one call (fasgd_apply_with_push_and_select) whose pass
+    # applies the push selected in the previous step (at its timestamp T) and
+    # then K client gradients (T + 1 ... T + K), taking the transmit decisions
+    # of this step's push from the v it leaves, followed by that selection's
+    # scan and scatter (the push is applied at T + K + 1 by the next pass).
+    # That is the order in which the server lock serialises the arrivals,
+    # and per step the work is K dense updates, one push selected and one
+    # push applied.  The first step of the warm-up has no push to apply; the
+    # push selected by the last timed step is applied after the timed
+    # region.  Each step's count goes to its own buffer, so the count of the
+    # push a pass applies stays readable.
     ev = {name: [] for name in ("pass", "select")}
     counts = []
-    pending = []                              # (client, grad_ts) of the selected, unapplied push
+    n_steps_all = warm + steps
+    cnts = torch.zeros(n_steps_all + 1, device=dev, dtype=torch.int64)
+    pending = []                              # (client, grad_ts, step) of the selected, unapplied push
 
-    def step(timed, c):
+    def step(i, timed, c):
         base = st.T                          # the schedule is indexed by server timestamp
         e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
+        p0 = torch.cuda.Event(enable_timing=True)
+        p1 = torch.cuda.Event(enable_timing=True)
         e2 = torch.cuda.Event(enable_timing=True)
         e0.record()
-        applied = None
+        out_cnt = cnts[i + 1:i + 2]
         if pending:
-            pc, pts = pending.pop()
+            pc, pts, j = pending.pop()
             sl = slice(base + 1, base + 1 + K)
-            fa.fasgd_apply_with_push(st, idx, val, cnt, seg, pc, pts, pool[:K], clients[sl], ts[sl])
-            applied = cnt.clone()            # entries applied, read before the next selection
+            T_sel = base + K + 1
+            fa.fasgd_record_next_pass(p0, p1)
+            fa.fasgd_apply_with_push_and_select(st, idx, val, cnts[j + 1:j + 2], seg, pc, pts, pool[:K],
+                                                clients[sl], ts[sl], pool[K], clients[T_sel], c, EPS_C, SEED,
+                                                idx, val, out_cnt, seg, ws)
+            applied = j + 1
         else:
             sl = slice(base, base + K)
             fa.fasgd_apply_updates(st, pool[:K], clients[sl], ts[sl])
-        e1.record()
-        T_sel = st.T
-        fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, T_sel, clients[T_sel], idx, val, cnt, ws,
-                                 seg_start=seg)
+            p1.record()
+            T_sel = st.T
+            fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, T_sel, clients[T_sel], idx, val, out_cnt, ws,
+                                     seg_start=seg)
+            applied = None
         e2.record()
-        pending.append((clients[T_sel], ts[T_sel]))
+        assert st.T == T_sel
+        pending.append((clients[T_sel], ts[T_sel], i))
         if timed:
-            ev["select"].append((e1, e2))
+            ev["select"].append((p1, e2))
             if applied is not None:
-                ev["pass"].append((e0, e1))
+                ev["pass"].append((p0, p1))
                 counts.append(applied)
 
     # the first dense pass gives v its scale; c is then fixed for the run
@@ -340,34 +353,38 @@ def main():
     c = calibrate_c(v, f)
     print(f"# c = {c:.6g} for transmit fraction {f}", file=sys.stderr, flush=True)
     for i in range(warm):
-        step(False, c)
+        step(i, False, c)
     torch.cuda.synchronize()
     print(f"# warmup done ({warm} steps)", file=sys.stderr, flush=True)
 
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
-        step(True, c)
+        step(warm + i, True, c)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     print(f"# timed {steps} steps in {wall:.3f} s", file=sys.stderr, flush=True)
     # the last push is applied after the timed region
-    pc, pts = pending.pop()
-    fa.bfasgd_apply_sparse(st, idx, val, cnt, pc, pts)
+    pc, pts, j = pending.pop()
+    fa.bfasgd_apply_sparse(st, idx, val, cnts[j + 1:j + 2], pc, pts)
+    cnt.copy_(cnts[j + 1:j + 2])
 
     ms = {k: [a.elapsed_time(b_) for a, b_ in pairs] for k, pairs in ev.items()}
-    m_list = [int(x.item()) for x in counts]
+    cnt_host = cnts.cpu().numpy()
+    m_list = [int(cnt_host[k]) for k in counts]
     m_avg = float(np.mean(m_list)) if m_list else 0.0
     updates = steps * P * K + sum(m_list)
     value = updates / wall
     pass_ms = float(np.mean(ms["pass"])) if ms["pass"] else float("nan")
-    # per launch: state 16 B read + 16 B write, 4 B per gradient, and for the
-    # push 4 B index + 4 B value per entry and its list index
-    pass_bytes = P * (32 + 4 * K) + 8 * m_avg + 4 * fa.bfasgd_list_index_length(P)
+    # per launch: state 16 B read + 16 B write, 4 B per gradient, for the
+    # push 4 B index + 4 B value per entry and its list index, and the next
+    # push's decisions (1 bit per parameter)
+    pass_bytes = P * (32 + 4 * K) + 8 * m_avg + 4 * fa.bfasgd_list_index_length(P) + P / 8
     achieved = pass_bytes / (pass_ms * 1e-3) / 1e9
     traffic = measured_traffic(P, K)
     sel_ms = float(np.mean(ms["select"]))
-    sel_bytes = P * 8 + m_avg * 8                   # v + g read, (idx, val) written
+    # after the pass took the decisions: ballots and g read, (idx, val) written
+    sel_bytes = P * 4 + P / 8 + m_avg * 8
 
     # the same steps as three separate calls (dense pass, selection, sparse
     # apply), for comparison
@@ -387,6 +404,23 @@ def main():
         sp_ms.append(e[2].elapsed_time(e[3]))
     sep_ms_avg = float(np.mean(sep_ms[1:]))
     sp_ms = float(np.mean(sp_ms[1:]))
+    # and as two calls: the pass with the queued push, then the full
+    # selection (which reads v again)
+    two_ms = []
+    fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, st.T, clients[st.T], idx, val, cnt, ws, seg_start=seg)
+    for r in range(3):
+        base = st.T
+        a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        fa.fasgd_apply_with_push(st, idx, val, cnt, seg, clients[base], ts[base], pool[:K],
+                                 clients[base + 1:base + 1 + K], ts[base + 1:base + 1 + K])
+        fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, st.T, clients[st.T], idx, val, cnt, ws,
+                                 seg_start=seg)
+        b_.record()
+        torch.cuda.synchronize()
+        two_ms.append(a.elapsed_time(b_))
+    fa.bfasgd_apply_sparse(st, idx, val, cnt, clients[st.T], ts[st.T])
+    two_ms_avg = float(np.mean(two_ms[1:]))
     sp_bytes = m_avg * 44                           # idx, val + 16 B state gather, 16 B scatter, 4 B last_T
 
     # SASGD mode of the same pass, measured after the timed region
@@ -506,15 +540,19 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic, "algorithmic_bytes": pass_bytes},
         "kernels": {
-            "fasgd_apply_with_push": {"ms": pass_ms, "GB/s": achieved,
-                                      "param_updates_per_s": (P * K + m_avg) / (pass_ms * 1e-3)},
+            "fasgd_apply_with_push_and_select": {
+                "pass_ms": pass_ms, "pass_GB/s": achieved,
+                "pass_param_updates_per_s": (P * K + m_avg) / (pass_ms * 1e-3),
+                "selection_after_the_pass_ms": sel_ms,
+                "selection_after_the_pass_GB/s": sel_bytes / (sel_ms * 1e-3) / 1e9},
+            "step_as_two_calls": {"ms": two_ms_avg,
+                                  "calls": "fasgd_apply_with_push, bfasgd_select_compact"},
             "fasgd_apply_updates": {"ms": dense_k[str(K)]["ms"] if str(K) in dense_k else None,
                                     "GB/s": dense_k[str(K)]["GB/s"] if str(K) in dense_k else None,
                                     "back_to_back_by_K": dense_k},
             "step_as_separate_calls": {"ms": sep_ms_avg,
                                        "calls": "fasgd_apply_updates, bfasgd_select_compact, bfasgd_apply_sparse"},
-            "bfasgd_select_compact": {"ms": sel_ms, "GB/s": sel_bytes / (sel_ms * 1e-3) / 1e9,
-                                      "ms_back_to_back": sel_b2b_ms,
+            "bfasgd_select_compact": {"ms_back_to_back": sel_b2b_ms,
                                       "GB/s_back_to_back": sel_b2b_bytes / (sel_b2b_ms * 1e-3) / 1e9,
                                       "frac_back_to_back": sel_b2b_bytes / (sel_b2b_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
                                       "transmitted_fraction": m_avg / P},

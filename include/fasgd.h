@@ -273,6 +273,35 @@ fasgd_status fasgd_apply_with_push(fasgd_state* st, const int32_t* push_idx, con
                                    const int64_t* grad_ts, int32_t K, hipStream_t stream);
 
 /*
+ * The server step of a pipeline: fasgd_apply_with_push (a queued push, then
+ * K gradients, in one pass), then the selection of the next push exactly as
+ * bfasgd_select_compact(st, next_grad, c, eps_c, seed, T', next_client,
+ * out_idx, out_val, out_capacity, out_count, out_seg_start, workspace,
+ * workspace_bytes) with T' = the timestamp after the pass (the one the next
+ * pass applies that push at) and v as the pass leaves it.  Every output
+ * (theta, n, b, v, T, dense_T, the list, its count and its index) is
+ * bit-identical to those two calls; when the state and the K gradients are
+ * 16-byte aligned the pass itself takes the next push's transmit decisions
+ * from the v it holds in registers, so the selection does not read v again.
+ * The output list may be the buffers of the push being applied (the pass
+ * reads them before the selection writes).
+ *   push_*, grads, clients, grad_ts, K  as for fasgd_apply_with_push
+ *   next_grad, next_client, c, eps_c, seed, out_*, workspace  as for
+ *                  bfasgd_select_compact
+ * Errors: those of the two calls it stands for; a rejected call enqueues
+ * nothing and leaves T alone.
+ */
+fasgd_status fasgd_apply_with_push_and_select(fasgd_state* st, const int32_t* push_idx, const float* push_val,
+                                              const int64_t* push_count, const uint32_t* push_seg_start,
+                                              int64_t push_capacity, int32_t push_client, int64_t push_grad_ts,
+                                              const float* const* grads, const int32_t* clients,
+                                              const int64_t* grad_ts, int32_t K, const float* next_grad,
+                                              int32_t next_client, float c, float eps_c, uint64_t seed,
+                                              int32_t* out_idx, float* out_val, int64_t out_capacity,
+                                              int64_t* out_count, uint32_t* out_seg_start, void* workspace,
+                                              size_t workspace_bytes, hipStream_t stream);
+
+/*
  * B compacted pushes applied in one pass (Sec. 2.3): the same state, T and
  * last_T, bit for bit, as B calls of bfasgd_apply_sparse in order b = 0 ..
  * B-1, push b at timestamp T + b with staleness T + b - grad_ts[b], but
@@ -372,6 +401,18 @@ const char* fasgd_status_string(fasgd_status s);
 
 /* Text describing the last error returned on the calling thread ("" if none). */
 const char* fasgd_last_error(void);
+
+/*
+ * Diagnostics: the next FASGD pass kernel this thread launches (through
+ * fasgd_apply_updates, fasgd_apply_with_push or
+ * fasgd_apply_with_push_and_select) records `start` on its stream just
+ * before the pass and `stop` just after it, so that the pass can be timed
+ * alone within a call that launches more kernels.  One-shot: the events are
+ * forgotten once recorded.  Both NULL clears a pending request; one NULL is
+ * FASGD_ERR_NULL.  The events are the caller's (created, and destroyed only
+ * after they are recorded or cleared).
+ */
+fasgd_status fasgd_record_next_pass(hipEvent_t start, hipEvent_t stop);
 
 #ifdef __cplusplus
 }

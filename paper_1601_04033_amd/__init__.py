@@ -37,7 +37,8 @@ ABI_FUNCTIONS = ("fasgd_init_state", "fasgd_apply_updates", "sasgd_apply_updates
                  "sgd_sync_apply", "bfasgd_apply_cached", "bfasgd_apply_fetch",
                  "bfasgd_segments_workspace_bytes", "bfasgd_decide_segments", "bfasgd_apply_segments",
                  "bfasgd_list_index_length", "fasgd_apply_with_push",
-                 "bfasgd_select_compact_batch", "fasgd_apply_pushes",
+                 "bfasgd_select_compact_batch", "fasgd_apply_pushes", "fasgd_apply_with_push_and_select",
+                 "fasgd_record_next_pass",
                  "fasgd_status_string", "fasgd_last_error")
 
 
@@ -80,6 +81,8 @@ def load_library(path: Optional[str] = None):
     lib.bfasgd_list_index_length.argtypes = [i64]
     lib.bfasgd_list_index_length.restype = i64
     lib.fasgd_apply_with_push.argtypes = [S, P, P, P, P, i64, i32, i64, P, P, P, i32, P]
+    lib.fasgd_apply_with_push_and_select.argtypes = [S, P, P, P, P, i64, i32, i64, P, P, P, i32,
+                                                     P, i32, f, f, u64, P, P, i64, P, P, P, sz, P]
     lib.bfasgd_apply_sparse.argtypes = [S, P, P, P, i64, i32, i64, P]
     lib.bfasgd_select_compact_batch.argtypes = [S, i32, P, f, f, u64, P, P, P, P, i64, P, P, P, sz, P]
     lib.fasgd_apply_pushes.argtypes = [S, i32, P, P, P, P, i64, P, P, P]
@@ -95,6 +98,7 @@ def load_library(path: Optional[str] = None):
                  "bfasgd_apply_cached", "bfasgd_apply_fetch", "bfasgd_decide_segments",
                  "bfasgd_apply_segments", "fasgd_apply_with_push"):
         getattr(lib, name).restype = ctypes.c_int
+    lib.fasgd_record_next_pass.argtypes = [P, P]
     lib.fasgd_status_string.argtypes = [ctypes.c_int]
     lib.fasgd_status_string.restype = ctypes.c_char_p
     lib.fasgd_last_error.argtypes = []
@@ -339,6 +343,49 @@ def fasgd_apply_pushes(state: State, idx, val, d_count, seg_start, clients: Sequ
         _dev_ptr(d_count, torch.int64, "d_count"), _batch_seg(seg_start, B, state.P, True), cap, cl, ts,
         _stream(stream))
     _check(rc)
+
+
+def fasgd_apply_with_push_and_select(state: State, push_idx, push_val, push_count, push_seg_start,
+                                     push_client: int, push_grad_ts: int, grads: Sequence, clients: Sequence[int],
+                                     grad_ts: Sequence[int], next_grad, next_client: int, c: float, eps_c: float,
+                                     seed: int, out_idx, out_val, out_count, out_seg_start, workspace,
+                                     stream=None) -> None:
+    """fasgd_apply_with_push, then the next push's selection (as
+    bfasgd_select_compact at the timestamp after the pass, from the v the
+    pass leaves) in one call; the output list may be the input push's
+    buffers.  T advances by K + 1."""
+    import torch
+    cap = push_idx.numel()
+    if push_val.numel() != cap:
+        raise ValueError("push_idx and push_val must have the same capacity")
+    out_cap = out_idx.numel()
+    if out_val.numel() != out_cap:
+        raise ValueError("out_idx and out_val must have the same capacity")
+    if next_grad.numel() != state.P:
+        raise ValueError("next_grad length differs from P")
+    ptrs, cl, t, K = _dense_args(state, grads, clients, grad_ts)
+    rc = load_library().fasgd_apply_with_push_and_select(
+        ctypes.byref(state.c), _dev_ptr(push_idx, torch.int32, "push_idx"),
+        _dev_ptr(push_val, torch.float32, "push_val"), _dev_ptr(push_count, torch.int64, "push_count"),
+        _seg_start_ptr(push_seg_start, state.P, required=True), cap, int(push_client), int(push_grad_ts),
+        ptrs, cl, t, K, _dev_ptr(next_grad, torch.float32, "next_grad"), int(next_client), c, eps_c,
+        int(seed) & (2 ** 64 - 1), _dev_ptr(out_idx, torch.int32, "out_idx"),
+        _dev_ptr(out_val, torch.float32, "out_val"), out_cap, _dev_ptr(out_count, torch.int64, "out_count"),
+        _seg_start_ptr(out_seg_start, state.P), _dev_ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
+        _stream(stream))
+    _check(rc)
+
+
+def fasgd_record_next_pass(start, stop) -> None:
+    """Record two torch.cuda.Events around the next FASGD pass kernel this
+    thread launches (diagnostics; both None clears).  The events are recorded
+    once here first, so that torch has created them."""
+    if start is None and stop is None:
+        _check(load_library().fasgd_record_next_pass(None, None))
+        return
+    start.record()
+    stop.record()
+    _check(load_library().fasgd_record_next_pass(int(start.cuda_event), int(stop.cuda_event)))
 
 
 def bfasgd_apply_sparse(state: State, idx, val, d_count, client: int, grad_ts: int, stream=None) -> None:

@@ -20,6 +20,8 @@
 //            index order), and writes the staged run at group offset + tile
 //            offset in contiguous stores.
 // The result depends only on (seed, T, client, v, grad), never on timing.
+#include <string.h>
+
 #include "kernels.hpp"
 
 // v_writelane_b32: write a wave-uniform value into one lane of a VGPR.  The
@@ -209,12 +211,26 @@ __device__ __forceinline__ void scan_groups(const SelectArgs& a, int64_t ng, boo
 // by the mark launch before this one) then scans the group totals itself.
 // Each arrival is a device-scope release, which costs more than a launch once
 // there are many groups; then select_top does that scan as its own launch.
-template <bool FUSED_TOP>
+// FROM_BALLOTS: the tile counts were not written (the mark step ran inside
+// another pass); count the tile's ballot bits instead.
+__device__ __forceinline__ uint32_t tile_bits(const uint64_t* tb)
+{
+    uint32_t n = 0;
+#pragma unroll
+    for (int k = 0; k < kTileWords; k += 2) {
+        const ulonglong2 w = *reinterpret_cast<const ulonglong2*>(tb + k);
+        n += __popcll(w.x) + __popcll(w.y);
+    }
+    return n;
+}
+
+template <bool FUSED_TOP, bool FROM_BALLOTS>
 __global__ __launch_bounds__(kScanBlock) void select_scan(const SelectArgs a0, const SelectBatch bt)
 {
     const SelectArgs a = push_args(a0, bt);
     const int64_t t = static_cast<int64_t>(blockIdx.x) * kScanBlock + threadIdx.x;
-    const uint32_t c = t < a.n_tiles ? a.tile_count[t] : 0u;
+    uint32_t c = 0;
+    if (t < a.n_tiles) c = FROM_BALLOTS ? tile_bits(a.ballots + t * kTileWords) : a.tile_count[t];
     uint32_t total;
     const uint32_t off = block_exclusive_scan(c, &total);
     if (t < a.n_tiles) a.tile_offset[t] = off;
@@ -440,9 +456,9 @@ hipError_t launch_select(const SelectArgs& a, const SelectBatch& bt, int B, bool
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (groups <= static_cast<unsigned>(kFusedTopGroups)) {
-        select_scan<true><<<dim3(groups, B), kScanBlock, 0, s>>>(a, bt);
+        select_scan<true, false><<<dim3(groups, B), kScanBlock, 0, s>>>(a, bt);
     } else {
-        select_scan<false><<<dim3(groups, B), kScanBlock, 0, s>>>(a, bt);
+        select_scan<false, false><<<dim3(groups, B), kScanBlock, 0, s>>>(a, bt);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         select_top<<<dim3(1, B), kScanBlock, 0, s>>>(a, bt);
@@ -450,6 +466,28 @@ hipError_t launch_select(const SelectArgs& a, const SelectBatch& bt, int B, bool
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     select_scatter<<<grid, kSelBlock, 0, s>>>(a, bt, aligned);
+    return hipGetLastError();
+}
+
+hipError_t launch_select_after_mark(const SelectArgs& a, bool aligned, hipStream_t s)
+{
+    const unsigned gx = static_cast<unsigned>((a.n_tiles + kWavesPerBlock - 1) / kWavesPerBlock);
+    const unsigned groups = static_cast<unsigned>((a.n_tiles + kScanBlock - 1) / kScanBlock);
+    if (groups > static_cast<unsigned>(kMaxGroups)) return hipErrorInvalidValue;
+    SelectBatch bt;
+    memset(&bt, 0, sizeof bt);
+    hipError_t e;
+    if (groups <= static_cast<unsigned>(kFusedTopGroups)) {
+        select_scan<true, true><<<groups, kScanBlock, 0, s>>>(a, bt);
+    } else {
+        select_scan<false, true><<<groups, kScanBlock, 0, s>>>(a, bt);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        select_top<<<1, kScanBlock, 0, s>>>(a, bt);
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    select_scatter<<<gx, kSelBlock, 0, s>>>(a, bt, aligned);
     return hipGetLastError();
 }
 

@@ -153,8 +153,13 @@ __device__ __forceinline__ void stage_push(const PushArgs& p, int64_t lo, int64_
     }
 }
 
-template <int MODE>
-__global__ __launch_bounds__(kBlock) void fasgd_dense_push_vec(const DenseArgs a, const PushArgs p)
+// MARK: the pass also takes the transmit decisions of the next push (Sec.
+// 2.3) from the v it leaves, i.e. the selection's mark step on the v that a
+// selection after the pass would read: one Philox call per chunk of 4, and
+// the segment's 4 ballot words (word c: bit c of each of the 64 chunks) in
+// the selection workspace, laid out as the mark launch lays them out.
+template <int MODE, bool MARK>
+__global__ __launch_bounds__(kBlock) void fasgd_dense_push_vec(const DenseArgs a, const PushArgs p, const SelectArgs m)
 {
     __shared__ float s_val[kWavesPerBlock][kPushSeg];
     __shared__ uint32_t s_flag[kWavesPerBlock][kWave];    // byte c of word l: parameter 4 l + c listed
@@ -235,7 +240,33 @@ __global__ __launch_bounds__(kBlock) void fasgd_dense_push_vec(const DenseArgs a
             if ((flags >> (8 * c)) & 0xffu) fasgd_step<MODE>(tt, nn, bb, vv, pv[c], p.coef, h);
             for (int k = 0; k < K; ++k) fasgd_step<MODE>(tt, nn, bb, vv, a.grad[k][j], a.coef[k], h);
             a.theta[j] = tt; a.n[j] = nn; a.b[j] = bb; a.v[j] = vv;
+            if (MARK) v[c] = vv;
         }
+    }
+    if (MARK) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) *m.groups_done = 0u;   // for the scan launch
+        const int n_own = own ? 4 : (i == nvec ? static_cast<int>(a.P - 4 * nvec) : 0);
+        uint32_t nib = 0;
+        if (n_own > 0) {
+            const uint64_t qg = m.chunk_base + static_cast<uint64_t>(i);   // global chunk index
+            const uint4 wd = philox4x32_10(
+                make_uint4(static_cast<uint32_t>(qg), static_cast<uint32_t>(qg >> 32), m.ctr_T, m.ctr_client),
+                m.key0, m.key1);
+            const uint32_t wds[4] = {wd.x, wd.y, wd.z, wd.w};
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                if (c < n_own) nib |= transmit_bit(wds[c], v[c], m.c, m.eps_c) << c;
+        }
+        uint64_t words[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) words[c] = __builtin_amdgcn_ballot_w64(((nib >> c) & 1u) != 0);
+        const int64_t tile_segs = m.n_tiles * 4;   // segments the ballot array holds
+        const uint64_t mine = lane == 0 ? words[0] : lane == 1 ? words[1] : lane == 2 ? words[2] : words[3];
+        if (seg < tile_segs && lane < 4) m.ballots[seg * 4 + lane] = mine;
+        // segments of the last tile beyond the grid hold no chunk: no bits
+        const int64_t last_seg = static_cast<int64_t>(gridDim.x) * kWavesPerBlock - 1;
+        if (seg == last_seg && lane < 4)
+            for (int64_t s2 = seg + 1; s2 < tile_segs; ++s2) m.ballots[s2 * 4 + lane] = 0;
     }
 }
 
@@ -389,23 +420,27 @@ void launch_dense_variant(const DenseArgs& a, bool aligned, unsigned grid, hipSt
 }
 
 template <int VARIANT>
-void launch_push_variant(const DenseArgs& a, const PushArgs& p, bool aligned, unsigned grid, hipStream_t s)
+void launch_push_variant(const DenseArgs& a, const PushArgs& p, const SelectArgs* m, bool aligned, unsigned grid,
+                         hipStream_t s)
 {
-    if (aligned)
-        fasgd_dense_push_vec<VARIANT><<<grid, kBlock, 0, s>>>(a, p);
+    if (m)
+        fasgd_dense_push_vec<VARIANT, true><<<grid, kBlock, 0, s>>>(a, p, *m);
+    else if (aligned)
+        fasgd_dense_push_vec<VARIANT, false><<<grid, kBlock, 0, s>>>(a, p, SelectArgs{});
     else
         fasgd_dense_push_scalar<VARIANT><<<grid, kBlock, 0, s>>>(a, p);
 }
 
-hipError_t launch_fasgd_dense_push(const DenseArgs& a, const PushArgs& p, int variant, bool aligned,
-                                   hipStream_t s)
+hipError_t launch_fasgd_dense_push(const DenseArgs& a, const PushArgs& p, const SelectArgs* mark, int variant,
+                                   bool aligned, hipStream_t s)
 {
+    if (mark && !aligned) return hipErrorInvalidValue;   // the decisions ride on the vector kernel only
     const unsigned grid = aligned ? grid_for((a.P >> 2) + 1) : grid_for(a.P);
     switch (variant) {
-    case kernel_variant(MATH_FAST, 0): launch_push_variant<kernel_variant(MATH_FAST, 0)>(a, p, aligned, grid, s); break;
-    case kernel_variant(MATH_IEEE, 0): launch_push_variant<kernel_variant(MATH_IEEE, 0)>(a, p, aligned, grid, s); break;
-    case kernel_variant(MATH_FAST, 1): launch_push_variant<kernel_variant(MATH_FAST, 1)>(a, p, aligned, grid, s); break;
-    case kernel_variant(MATH_IEEE, 1): launch_push_variant<kernel_variant(MATH_IEEE, 1)>(a, p, aligned, grid, s); break;
+    case kernel_variant(MATH_FAST, 0): launch_push_variant<kernel_variant(MATH_FAST, 0)>(a, p, mark, aligned, grid, s); break;
+    case kernel_variant(MATH_IEEE, 0): launch_push_variant<kernel_variant(MATH_IEEE, 0)>(a, p, mark, aligned, grid, s); break;
+    case kernel_variant(MATH_FAST, 1): launch_push_variant<kernel_variant(MATH_FAST, 1)>(a, p, mark, aligned, grid, s); break;
+    case kernel_variant(MATH_IEEE, 1): launch_push_variant<kernel_variant(MATH_IEEE, 1)>(a, p, mark, aligned, grid, s); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

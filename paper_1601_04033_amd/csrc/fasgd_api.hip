@@ -15,6 +15,24 @@ namespace {
 
 thread_local char g_err[512];
 
+// fasgd_record_next_pass: events recorded around the next FASGD pass kernel
+// this thread launches (one-shot)
+thread_local hipEvent_t g_pass_start = nullptr;
+thread_local hipEvent_t g_pass_stop = nullptr;
+
+hipError_t pass_begin(hipStream_t stream)
+{
+    return g_pass_start ? hipEventRecord(g_pass_start, stream) : hipSuccess;
+}
+
+hipError_t pass_end(hipStream_t stream)
+{
+    if (!g_pass_stop) return hipSuccess;
+    const hipError_t e = hipEventRecord(g_pass_stop, stream);
+    g_pass_start = g_pass_stop = nullptr;
+    return e;
+}
+
 fasgd_status fail(fasgd_status s, const char* fmt, ...)
 {
     va_list ap;
@@ -208,7 +226,9 @@ fasgd_status fasgd_apply_updates(fasgd_state* st, const float* const* grads, con
     bool vec = false;
     fasgd_status s = dense_common(st, grads, clients, grad_ts, K, true, a, vec);
     if (s != FASGD_OK) return s;
-    const hipError_t e = fasgd::launch_fasgd_dense(a, variant_of(st), vec, stream);
+    hipError_t e = pass_begin(stream);
+    if (e == hipSuccess) e = fasgd::launch_fasgd_dense(a, variant_of(st), vec, stream);
+    if (e == hipSuccess) e = pass_end(stream);
     if (e != hipSuccess) return hip_fail(e, "fasgd_apply_updates");
     st->dense_T = st->T + K - 1;
     st->T += K;
@@ -243,12 +263,13 @@ int64_t bfasgd_list_index_length(int64_t P)
 
 namespace {
 
-// Checks and launch of B selections; push b's per-push arguments are
-// grads[b], T[b], clients[b].
-fasgd_status select_common(const fasgd_state* st, int32_t B, const float* const* grads, float c, float eps_c,
-                           uint64_t seed, const int64_t* T, const int32_t* clients, int32_t* out_idx,
-                           float* out_val, int64_t capacity, int64_t* d_count, uint32_t* out_seg_start,
-                           void* workspace, size_t workspace_bytes, hipStream_t stream, const char* what)
+// Checks and kernel arguments of B selections; push b's per-push arguments
+// are grads[b], T[b], clients[b].  vec: v and every gradient 16-byte aligned.
+fasgd_status select_setup(const fasgd_state* st, int32_t B, const float* const* grads, float c, float eps_c,
+                          uint64_t seed, const int64_t* T, const int32_t* clients, int32_t* out_idx,
+                          float* out_val, int64_t capacity, int64_t* d_count, uint32_t* out_seg_start,
+                          void* workspace, size_t workspace_bytes, fasgd::SelectArgs& a, fasgd::SelectBatch& bt,
+                          bool& vec)
 {
     if (!st) return fail(FASGD_ERR_NULL, "state is NULL");
     if (st->P < 1 || st->P > INT32_MAX) return fail(FASGD_ERR_ARG, "P must be in [1, INT32_MAX] for int32 indices");
@@ -278,11 +299,9 @@ fasgd_status select_common(const fasgd_state* st, int32_t B, const float* const*
     if (workspace_bytes / size_t(B) < per_push)
         return fail(FASGD_ERR_CAPACITY, "workspace of %zu bytes is smaller than the %zu needed", workspace_bytes,
                     per_push * size_t(B));
-    fasgd::SelectArgs a;
     memset(&a, 0, sizeof a);
-    fasgd::SelectBatch bt;
     memset(&bt, 0, sizeof bt);
-    bool vec = aligned(st->v, 16);
+    vec = aligned(st->v, 16);
     for (int32_t p = 0; p < B; ++p) {
         bt.grad[p] = grads[p];
         bt.ctr_T[p] = static_cast<uint32_t>(T[p]);
@@ -309,6 +328,20 @@ fasgd_status select_common(const fasgd_state* st, int32_t B, const float* const*
     bt.list_stride = capacity;
     bt.index_stride = a.n_segs + 1;
     bt.ws_stride = per_push;
+    return FASGD_OK;
+}
+
+fasgd_status select_common(const fasgd_state* st, int32_t B, const float* const* grads, float c, float eps_c,
+                           uint64_t seed, const int64_t* T, const int32_t* clients, int32_t* out_idx,
+                           float* out_val, int64_t capacity, int64_t* d_count, uint32_t* out_seg_start,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream, const char* what)
+{
+    fasgd::SelectArgs a;
+    fasgd::SelectBatch bt;
+    bool vec = false;
+    const fasgd_status s = select_setup(st, B, grads, c, eps_c, seed, T, clients, out_idx, out_val, capacity,
+                                        d_count, out_seg_start, workspace, workspace_bytes, a, bt, vec);
+    if (s != FASGD_OK) return s;
     const hipError_t e = fasgd::launch_select(a, bt, B, vec, stream);
     if (e != hipSuccess) return hip_fail(e, what);
     return ok();
@@ -371,10 +404,14 @@ fasgd_status bfasgd_apply_sparse(fasgd_state* st, const int32_t* idx, const floa
     return ok();
 }
 
-fasgd_status fasgd_apply_with_push(fasgd_state* st, const int32_t* push_idx, const float* push_val,
-                                   const int64_t* push_count, const uint32_t* push_seg_start, int64_t capacity,
-                                   int32_t push_client, int64_t push_grad_ts, const float* const* grads,
-                                   const int32_t* clients, const int64_t* grad_ts, int32_t K, hipStream_t stream)
+namespace {
+
+// Checks and kernel arguments of a push followed by K gradients in one pass.
+fasgd_status with_push_setup(fasgd_state* st, const int32_t* push_idx, const float* push_val,
+                             const int64_t* push_count, const uint32_t* push_seg_start, int64_t capacity,
+                             int32_t push_client, int64_t push_grad_ts, const float* const* grads,
+                             const int32_t* clients, const int64_t* grad_ts, int32_t K, fasgd::DenseArgs& a,
+                             fasgd::PushArgs& p, bool& vec)
 {
     fasgd_status s = check_state(st, true);
     if (s != FASGD_OK) return s;
@@ -390,11 +427,8 @@ fasgd_status fasgd_apply_with_push(fasgd_state* st, const int32_t* push_idx, con
     // the K gradients follow the push: they are applied at T + 1 ... T + K
     fasgd_state after = *st;
     after.T = st->T + 1;
-    fasgd::DenseArgs a;
-    bool vec = false;
     s = dense_common(&after, grads, clients, grad_ts, K, true, a, vec);
     if (s != FASGD_OK) return s;
-    fasgd::PushArgs p;
     memset(&p, 0, sizeof p);
     p.idx = push_idx;
     p.val = push_val;
@@ -403,8 +437,71 @@ fasgd_status fasgd_apply_with_push(fasgd_state* st, const int32_t* push_idx, con
     p.capacity = capacity;
     p.n_segs = fasgd::push_segments(st->P);
     p.coef = st->math_mode == FASGD_MATH_FAST ? st->alpha / push_tau : push_tau;
-    const hipError_t e = fasgd::launch_fasgd_dense_push(a, p, variant_of(st), vec, stream);
+    return FASGD_OK;
+}
+
+}  // namespace
+
+fasgd_status fasgd_apply_with_push(fasgd_state* st, const int32_t* push_idx, const float* push_val,
+                                   const int64_t* push_count, const uint32_t* push_seg_start, int64_t capacity,
+                                   int32_t push_client, int64_t push_grad_ts, const float* const* grads,
+                                   const int32_t* clients, const int64_t* grad_ts, int32_t K, hipStream_t stream)
+{
+    fasgd::DenseArgs a;
+    fasgd::PushArgs p;
+    bool vec = false;
+    const fasgd_status s = with_push_setup(st, push_idx, push_val, push_count, push_seg_start, capacity,
+                                           push_client, push_grad_ts, grads, clients, grad_ts, K, a, p, vec);
+    if (s != FASGD_OK) return s;
+    hipError_t e = pass_begin(stream);
+    if (e == hipSuccess) e = fasgd::launch_fasgd_dense_push(a, p, nullptr, variant_of(st), vec, stream);
+    if (e == hipSuccess) e = pass_end(stream);
     if (e != hipSuccess) return hip_fail(e, "fasgd_apply_with_push");
+    st->dense_T = st->T + K;
+    st->T += K + 1;
+    return ok();
+}
+
+fasgd_status fasgd_apply_with_push_and_select(fasgd_state* st, const int32_t* push_idx, const float* push_val,
+                                              const int64_t* push_count, const uint32_t* push_seg_start,
+                                              int64_t push_capacity, int32_t push_client, int64_t push_grad_ts,
+                                              const float* const* grads, const int32_t* clients,
+                                              const int64_t* grad_ts, int32_t K, const float* next_grad,
+                                              int32_t next_client, float c, float eps_c, uint64_t seed,
+                                              int32_t* out_idx, float* out_val, int64_t out_capacity,
+                                              int64_t* out_count, uint32_t* out_seg_start, void* workspace,
+                                              size_t workspace_bytes, hipStream_t stream)
+{
+    fasgd::DenseArgs a;
+    fasgd::PushArgs p;
+    bool vec = false;
+    fasgd_status s = with_push_setup(st, push_idx, push_val, push_count, push_seg_start, push_capacity,
+                                     push_client, push_grad_ts, grads, clients, grad_ts, K, a, p, vec);
+    if (s != FASGD_OK) return s;
+    // the next push is applied at the timestamp after the pass, and decided
+    // from the v the pass leaves
+    fasgd_state after = *st;
+    after.T = st->T + K + 1;
+    const int64_t T_next = after.T;
+    fasgd::SelectArgs m;
+    fasgd::SelectBatch bt;
+    bool sel_vec = false;
+    s = select_setup(&after, 1, &next_grad, c, eps_c, seed, &T_next, &next_client, out_idx, out_val, out_capacity,
+                     out_count, out_seg_start, workspace, workspace_bytes, m, bt, sel_vec);
+    if (s != FASGD_OK) return s;
+    hipError_t e = pass_begin(stream);
+    if (vec) {
+        // the pass takes the decisions; the selection's own launches scan
+        // them and scatter
+        if (e == hipSuccess) e = fasgd::launch_fasgd_dense_push(a, p, &m, variant_of(st), true, stream);
+        if (e == hipSuccess) e = pass_end(stream);
+        if (e == hipSuccess) e = fasgd::launch_select_after_mark(m, aligned(next_grad, 16), stream);
+    } else {
+        if (e == hipSuccess) e = fasgd::launch_fasgd_dense_push(a, p, nullptr, variant_of(st), false, stream);
+        if (e == hipSuccess) e = pass_end(stream);
+        if (e == hipSuccess) e = fasgd::launch_select(m, bt, 1, sel_vec, stream);
+    }
+    if (e != hipSuccess) return hip_fail(e, "fasgd_apply_with_push_and_select");
     st->dense_T = st->T + K;
     st->T += K + 1;
     return ok();
@@ -637,5 +734,13 @@ const char* fasgd_status_string(fasgd_status s)
 }
 
 const char* fasgd_last_error(void) { return g_err; }
+
+fasgd_status fasgd_record_next_pass(hipEvent_t start, hipEvent_t stop)
+{
+    if ((start == nullptr) != (stop == nullptr)) return fail(FASGD_ERR_NULL, "start and stop: both or neither");
+    g_pass_start = start;
+    g_pass_stop = stop;
+    return ok();
+}
 
 }  // extern "C"

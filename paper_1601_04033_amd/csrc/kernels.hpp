@@ -77,6 +77,10 @@ size_t select_workspace_bytes(int64_t P);
 // Carve the workspace into ballots / tile counts / tile offsets.
 void select_workspace_layout(void* ws, int64_t P, SelectArgs& a);
 hipError_t launch_select(const SelectArgs& a, const SelectBatch& bt, int B, bool aligned, hipStream_t s);
+// The selection after its mark step was taken elsewhere (ballot words in the
+// workspace, tile counts not written): scan with the counts taken from the
+// ballots, then scatter.  One push.
+hipError_t launch_select_after_mark(const SelectArgs& a, bool aligned, hipStream_t s);
 
 struct SparseArgs {
     float* theta;
@@ -112,8 +116,10 @@ struct PushArgs {
     float coef;             // as DenseArgs::coef for the push
 };
 
-hipError_t launch_fasgd_dense_push(const DenseArgs& a, const PushArgs& p, int variant, bool aligned,
-                                   hipStream_t s);
+// mark: optional; the selection arguments of the next push, whose transmit
+// decisions the pass then takes from the v it leaves (vector path only).
+hipError_t launch_fasgd_dense_push(const DenseArgs& a, const PushArgs& p, const SelectArgs* mark, int variant,
+                                   bool aligned, hipStream_t s);
 
 // B compacted pushes applied in order in one pass (push b at timestamp
 // T0 + b); listed parameters get last_T = T0 + the last push that lists them.

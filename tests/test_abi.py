@@ -289,6 +289,43 @@ def test_apply_pushes_rejects_bad_arguments(lib):
     assert ap(cap=0) == 0 and st.T == 4  # nothing to apply: T still advances by B
 
 
+def test_push_and_select_rejects_bad_arguments(lib):
+    """The pass-and-select call checks the pass's arguments and the next
+    selection's (at the timestamp after the pass) before enqueueing anything."""
+    st, f = _state(P=16, T=2)
+    cnt = np.zeros(4, np.int64)
+    cntp = (cnt.ctypes.data + 7) & ~7
+    ws_need = fa.bfasgd_workspace_bytes(16)
+    ws = np.zeros(ws_need + 512, np.uint8)
+    wsp = (ws.ctypes.data + 255) & ~255
+
+    def ps(pts=0, ts=(0,), nc=0, c=1.0, ws_bytes=ws_need, next_grad="ok", out_count=cntp + 8):
+        K = len(ts)
+        g = (ctypes.c_void_p * K)(*([f.ptr(5)] * K))
+        cl = (ctypes.c_int32 * K)(*([0] * K))
+        t = (ctypes.c_int64 * K)(*ts)
+        ng = f.ptr(5) if next_grad == "ok" else next_grad
+        return lib.fasgd_apply_with_push_and_select(ctypes.byref(st), f.ptr(0), f.ptr(1), cntp, f.ptr(3), 16, 0,
+                                                    pts, g, cl, t, K, ng, nc, c, 1e-8, 7, f.ptr(2), f.ptr(4), 16,
+                                                    out_count, None, wsp, ws_bytes, None)
+
+    assert ps(pts=3) == 3                  # the push is applied at T = 2
+    assert ps(ts=(4,)) == 3                # the gradient at T + 1 = 3
+    assert ps(nc=4) == 4                   # next client outside [0, lambda)
+    assert ps(c=-1.0) == 2
+    assert ps(ws_bytes=ws_need - 1) == 6
+    assert ps(next_grad=None) == 1
+    assert ps(out_count=cntp + 4) == 5
+    assert st.T == 2 and st.dense_T == -1
+
+
+def test_record_next_pass_takes_both_events_or_none(lib):
+    fake = np.zeros(4, np.int64)
+    assert lib.fasgd_record_next_pass(fake.ctypes.data, None) == 1
+    assert lib.fasgd_record_next_pass(None, fake.ctypes.data) == 1
+    assert lib.fasgd_record_next_pass(None, None) == 0
+
+
 def test_sparse_rejects_bad_arguments(lib):
     st, f = _state(P=16, T=2)
     cnt = np.zeros(2, np.int64)

@@ -3,7 +3,9 @@
 bit-identity of theta, n, b, v with the two separate calls it stands for
 (bfasgd_apply_sparse, then fasgd_apply_updates) and the same last update of
 every parameter, and parity with the oracle applying the push and then the
-K gradients one by one."""
+K gradients one by one.  The same pass followed by the next push's selection
+(fasgd_apply_with_push_and_select, whose pass takes the transmit decisions
+itself) against fasgd_apply_with_push and then bfasgd_select_compact."""
 import numpy as np
 import pytest
 
@@ -34,7 +36,7 @@ def _states(P, dev, mode, reading, seed, offset=0):
     T = 5) and the oracle state holding the same values; offset = 1 places the
     arrays 4 bytes into their buffers (the scalar path)."""
     import torch
-    w = workload.WORKLOADS["mlp_bfasgd"]
+    w = workload.WORKLOADS["mlp_bfasgd" if P <= workload.MLP_P else "large"]
     theta0, m_, s_ = workload.host_params(w, P, seed=seed)
     b0 = m_ + s_ * np.float32(0.1)
     n0 = (b0 * b0 + s_ * s_).astype(np.float32)
@@ -154,3 +156,79 @@ def test_push_inside_pass_matches_oracle():
     assert int(cnt.item()) == r_m
     assert_state_close(st, ref, RTOL_SEQ, what="push then 16 gradients")
     assert (st.last_T.cpu() == -1).all() and st.dense_T == 5 + K
+
+
+def _selection_buffers(P, cap, dev):
+    import torch
+    return (torch.full((max(cap, 1),), -1, device=dev, dtype=torch.int32)[:cap],
+            torch.zeros(max(cap, 1), device=dev)[:cap], torch.zeros(1, device=dev, dtype=torch.int64),
+            torch.full((fa.bfasgd_list_index_length(P),), -1, device=dev, dtype=torch.int32),
+            fa.allocate_workspace(P, dev))
+
+
+@pytest.mark.parametrize("P,K,offset,cap_frac,base", [
+    (1, 1, 0, 1.0, 0), (255, 3, 0, 1.0, 0), (257, 8, 0, 1.0, 0), (1027, 2, 0, 1.0, 4096),
+    (100_003, 8, 0, 1.0, 0), (100_003, 8, 0, 0.03, 0), (262_144, 4, 0, 1.0, 0), (262_145, 4, 0, 1.0, 8),
+    (1_000_003, 33, 0, 1.0, 0), (65_537, 5, 1, 1.0, 0), (67_108_869, 2, 0, 1.0, 0)])
+@pytest.mark.parametrize("mode", [fa.MATH_FAST, fa.MATH_IEEE])
+def test_push_pass_and_next_selection_are_bit_identical(P, K, offset, cap_frac, base, mode):
+    """fasgd_apply_with_push_and_select against fasgd_apply_with_push, then
+    bfasgd_select_compact at the timestamp after the pass: the state, T,
+    dense_T, the next push's count, list and list index bit for bit.  Covers
+    ragged tails, P a multiple of 1024 (the thread after the last chunk
+    starts a segment past the ballot array), a shard offset, a capacity cut,
+    arrays 4 bytes off alignment (pass and selection as separate launches)
+    and more than 64 scan groups."""
+    import torch
+    dev = gpu()
+    a, b, _, (m_, s_, w), keep = _states(P, dev, mode, fa.V_EQUATIONS, seed=P % 991, offset=offset)
+    a.c.index_base = b.c.index_base = base
+    g_push = to_dev(workload.host_gradient(w, m_, s_, 5, seed=2), dev)
+    gs = [to_dev(workload.host_gradient(w, m_, s_, 6 + k, seed=2), dev) for k in range(K)]
+    g_next = to_dev(workload.host_gradient(w, m_, s_, 6 + K, seed=2), dev)
+    clients, ts = [k % w.lam for k in range(K)], [max(6 + k - 2, 0) for k in range(K)]
+    idx, val, cnt, seg = _select(a, g_push, 100.0, 5, 1, dev)
+    cap = max(1, int(P * cap_frac))
+    A = _selection_buffers(P, cap, dev)
+    B = _selection_buffers(P, cap, dev)
+    fa.fasgd_apply_with_push(a, idx, val, cnt, seg, 1, 4, gs, clients, ts)
+    fa.bfasgd_select_compact(a, g_next, 60.0, 1e-8, SEED, a.T, 2, A[0], A[1], A[2], A[4], seg_start=A[3])
+    fa.fasgd_apply_with_push_and_select(b, idx, val, cnt, seg, 1, 4, gs, clients, ts, g_next, 2, 60.0, 1e-8, SEED,
+                                        B[0], B[1], B[2], B[3], B[4])
+    _assert_same(a, b)
+    assert b.T == 5 + K + 1
+    m = int(A[2].item())
+    assert int(B[2].item()) == m
+    u = min(m, cap)
+    assert torch.equal(A[0][:u], B[0][:u])
+    assert torch.equal(A[1][:u].view(torch.int32), B[1][:u].view(torch.int32))
+    assert torch.equal(A[3], B[3])
+    if cap_frac == 1.0:
+        assert (B[0][u:] == -1).all()
+        assert 0.02 * P < m < 0.6 * P or P < 300
+
+
+def test_push_pass_and_next_selection_into_the_applied_lists():
+    """The next push's list written into the buffers of the push the pass
+    applies (the pipeline's use), against the two calls with separate buffers."""
+    import torch
+    dev = gpu()
+    P, K = 300_007, 8
+    a, b, _, (m_, s_, w), keep = _states(P, dev, fa.MATH_FAST, fa.V_EQUATIONS, seed=17)
+    g_push = to_dev(workload.host_gradient(w, m_, s_, 5, seed=17), dev)
+    gs = [to_dev(workload.host_gradient(w, m_, s_, 6 + k, seed=17), dev) for k in range(K)]
+    g_next = to_dev(workload.host_gradient(w, m_, s_, 6 + K, seed=17), dev)
+    clients, ts = [k % w.lam for k in range(K)], [6 + k - 1 for k in range(K)]
+    ia, va, ca, sa = _select(a, g_push, 100.0, 5, 1, dev)
+    ib, vb, cb, sb = (x.clone() for x in (ia, va, ca, sa))
+    A = _selection_buffers(P, P, dev)
+    fa.fasgd_apply_with_push(a, ia, va, ca, sa, 1, 4, gs, clients, ts)
+    fa.bfasgd_select_compact(a, g_next, 60.0, 1e-8, SEED, a.T, 2, A[0], A[1], A[2], A[4], seg_start=A[3])
+    ws = fa.allocate_workspace(P, dev)
+    fa.fasgd_apply_with_push_and_select(b, ib, vb, cb, sb, 1, 4, gs, clients, ts, g_next, 2, 60.0, 1e-8, SEED,
+                                        ib, vb, cb, sb, ws)
+    _assert_same(a, b)
+    m = int(A[2].item())
+    assert int(cb.item()) == m
+    assert torch.equal(A[0][:m], ib[:m]) and torch.equal(A[1][:m], vb[:m]) and torch.equal(A[3], sb)
+
