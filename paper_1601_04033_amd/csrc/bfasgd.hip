@@ -212,16 +212,33 @@ __device__ __forceinline__ void scan_groups(const SelectArgs& a, int64_t ng, boo
 // Each arrival is a device-scope release, which costs more than a launch once
 // there are many groups; then select_top does that scan as its own launch.
 // FROM_BALLOTS: the tile counts were not written (the mark step ran inside
-// another pass); count the tile's ballot bits instead.
-__device__ __forceinline__ uint32_t tile_bits(const uint64_t* tb)
+// another pass); count the tiles' ballot bits instead.  The wave's 64 tiles
+// are 8 KB of ballot words, read in 8 rounds of one 16-byte piece per lane
+// (8 lanes per tile, contiguous), summed over each group of 8 lanes and
+// passed through LDS to the lane of the tile.
+__device__ __forceinline__ uint32_t wave_tile_bits(const SelectArgs& a, int64_t wave_first_tile, int lane)
 {
-    uint32_t n = 0;
+    __shared__ uint32_t s_cnt[kScanBlock / kWave][kWave];
+    const int w = threadIdx.x / kWave;
+    constexpr int kPieces = kTileWords / 2;                 // 16-byte pieces per tile
+    constexpr int kTilesPerRound = kWave / kPieces;
+    const ulonglong2* base = reinterpret_cast<const ulonglong2*>(a.ballots + wave_first_tile * kTileWords);
 #pragma unroll
-    for (int k = 0; k < kTileWords; k += 2) {
-        const ulonglong2 w = *reinterpret_cast<const ulonglong2*>(tb + k);
-        n += __popcll(w.x) + __popcll(w.y);
+    for (int r = 0; r < kPieces; ++r) {
+        const int t = r * kTilesPerRound + lane / kPieces;  // tile of this lane's piece, within the wave's 64
+        uint32_t n = 0;
+        if (wave_first_tile + t < a.n_tiles) {
+            const ulonglong2 piece = base[r * kWave + lane];
+            n = __popcll(piece.x) + __popcll(piece.y);
+        }
+#pragma unroll
+        for (int d = 1; d < kPieces; d <<= 1) n += __shfl_xor(n, d, kWave);
+        if (lane % kPieces == 0) s_cnt[w][t] = n;
     }
-    return n;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    return s_cnt[w][lane];
 }
 
 template <bool FUSED_TOP, bool FROM_BALLOTS>
@@ -230,7 +247,13 @@ __global__ __launch_bounds__(kScanBlock) void select_scan(const SelectArgs a0, c
     const SelectArgs a = push_args(a0, bt);
     const int64_t t = static_cast<int64_t>(blockIdx.x) * kScanBlock + threadIdx.x;
     uint32_t c = 0;
-    if (t < a.n_tiles) c = FROM_BALLOTS ? tile_bits(a.ballots + t * kTileWords) : a.tile_count[t];
+    if (FROM_BALLOTS) {
+        const int64_t wave_first = t - (threadIdx.x & (kWave - 1));
+        c = wave_tile_bits(a, wave_first, threadIdx.x & (kWave - 1));
+        if (t >= a.n_tiles) c = 0;
+    } else if (t < a.n_tiles) {
+        c = a.tile_count[t];
+    }
     uint32_t total;
     const uint32_t off = block_exclusive_scan(c, &total);
     if (t < a.n_tiles) a.tile_offset[t] = off;
