@@ -232,3 +232,28 @@ def test_push_pass_and_next_selection_into_the_applied_lists():
     assert int(cb.item()) == m
     assert torch.equal(A[0][:m], ib[:m]) and torch.equal(A[1][:m], vb[:m]) and torch.equal(A[3], sb)
 
+
+@pytest.mark.parametrize("mode", [fa.MATH_FAST, fa.MATH_IEEE])
+def test_push_pass_and_next_selection_prose_reading(mode):
+    """The same bit-identity with the text's reading of v (the decisions use
+    whichever v the state keeps)."""
+    import torch
+    dev = gpu()
+    P, K = 200_003, 6
+    a, b, _, (m_, s_, w), keep = _states(P, dev, mode, fa.V_PROSE, seed=29)
+    g_push = to_dev(workload.host_gradient(w, m_, s_, 5, seed=29), dev)
+    gs = [to_dev(workload.host_gradient(w, m_, s_, 6 + k, seed=29), dev) for k in range(K)]
+    g_next = to_dev(workload.host_gradient(w, m_, s_, 6 + K, seed=29), dev)
+    clients, ts = [k % w.lam for k in range(K)], [6 + k for k in range(K)]
+    idx, val, cnt, seg = _select(a, g_push, 100.0, 5, 1, dev)
+    A = _selection_buffers(P, P, dev)
+    B = _selection_buffers(P, P, dev)
+    fa.fasgd_apply_with_push(a, idx, val, cnt, seg, 1, 5, gs, clients, ts)
+    fa.bfasgd_select_compact(a, g_next, 5.0, 1e-8, SEED, a.T, 3, A[0], A[1], A[2], A[4], seg_start=A[3])
+    fa.fasgd_apply_with_push_and_select(b, idx, val, cnt, seg, 1, 5, gs, clients, ts, g_next, 3, 5.0, 1e-8, SEED,
+                                        B[0], B[1], B[2], B[3], B[4])
+    _assert_same(a, b)
+    m = int(A[2].item())
+    assert int(B[2].item()) == m and 0 < m < P
+    assert torch.equal(A[0][:m], B[0][:m]) and torch.equal(A[3], B[3])
+
