@@ -68,18 +68,20 @@ def _batch_buffers(B, P, cap, dev):
     return idx, val, cnt, seg, ws
 
 
-@pytest.mark.parametrize("P,B,cap_frac,offset", [
-    (1, 3, 1.0, 0), (1027, 16, 1.0, 0), (100_003, 16, 1.0, 0), (100_003, 5, 0.05, 0),
-    (1_000_003, 64, 1.0, 0), (65_537, 7, 1.0, 1), (17_000_003, 3, 1.0, 0)])
-def test_batch_select_equals_single_selects(P, B, cap_frac, offset):
+@pytest.mark.parametrize("P,B,cap_frac,offset,base", [
+    (1, 3, 1.0, 0, 0), (1027, 16, 1.0, 0, 0), (100_003, 16, 1.0, 0, 0), (100_003, 5, 0.05, 0, 0),
+    (100_003, 6, 1.0, 0, 4 * 123_457), (1_000_003, 64, 1.0, 0, 0), (65_537, 7, 1.0, 1, 0),
+    (17_000_003, 3, 1.0, 0, 0)])
+def test_batch_select_equals_single_selects(P, B, cap_frac, offset, base):
     """Push by push, the batch gives the count, list and list index of a
     single selection with the same gradient, T and client, bit for bit
-    (including a capacity cut, the scalar path for gradients 4 bytes off
-    16-byte alignment, 64 pushes, and 17M parameters, where the group scan
-    takes its two-launch form)."""
+    (including a capacity cut, a shard offset, the scalar path for gradients
+    4 bytes off 16-byte alignment, 64 pushes, and 17M parameters, where the
+    group scan takes its two-launch form)."""
     import torch
     dev = gpu()
     (st,), _, (m_, s_, w), keep = _mid_run_state(P, dev, seed=P % 977, copies=1)
+    st.c.index_base = base                   # a shard's global offset keys the draws
     grads = _gradients(B, P, m_, s_, w, dev, seed=5, offset=offset)
     Ts = [40 + 3 * k for k in range(B)]
     clients = [(5 * k + 1) % w.lam for k in range(B)]

@@ -42,8 +42,10 @@ def _same(a, b, what):
 
 def test_replayed_push_batches_and_dense_passes_match_eager():
     """One graph holding a batched selection, the batched apply, a K = 4
-    FASGD pass, a selection with its list index and the pass that applies
-    that push before 2 more gradients; replayed three times."""
+    FASGD pass, a selection with its list index, the pass that applies that
+    push before 2 more gradients, and the pass that applies the same list
+    before 3 more and selects the next push into those buffers; replayed
+    three times."""
     import torch
     dev = gpu()
     P, B = 200_003, 4
@@ -73,6 +75,10 @@ def test_replayed_push_batches_and_dense_passes_match_eager():
                                  bf["cnt"][0:1], bf["ws"], seg_start=bf["seg"][0])
         fa.fasgd_apply_with_push(st, bf["idx"][0], bf["val"][0], bf["cnt"][0:1], bf["seg"][0], 5, T - 1,
                                  grads[1:3], [6, 7], [T, T - 1])
+        T = st.T
+        fa.fasgd_apply_with_push_and_select(st, bf["idx"][0], bf["val"][0], bf["cnt"][0:1], bf["seg"][0], 8, T - 3,
+                                            grads[3:6], [1, 2, 3], [T, T, T - 2], grads[6], 9, 40.0, 1e-8, SEED,
+                                            bf["idx"][0], bf["val"][0], bf["cnt"][0:1], bf["seg"][0], bf["ws"])
 
     torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
@@ -91,5 +97,6 @@ def test_replayed_push_batches_and_dense_passes_match_eager():
         _same(gs, es, f"replay {r}")
         for key in ("cnt", "seg"):
             assert torch.equal(gb[key], eb[key]), f"replay {r}: {key}"
-        m = int(eb["cnt"][1].item())
-        assert torch.equal(gb["idx"][1, :m], eb["idx"][1, :m]), f"replay {r}: list"
+        for k in (0, 1):
+            m = int(eb["cnt"][k].item())
+            assert torch.equal(gb["idx"][k, :m], eb["idx"][k, :m]), f"replay {r}: list {k}"
