@@ -408,7 +408,8 @@ const char* fasgd_last_error(void);
  * fasgd_apply_with_push_and_select) records `start` on its stream just
  * before the pass and `stop` just after it, so that the pass can be timed
  * alone within a call that launches more kernels.  One-shot: the events are
- * forgotten once recorded.  Both NULL clears a pending request; one NULL is
+ * forgotten once recorded; a call rejected before its pass leaves the
+ * request pending.  Both NULL clears a pending request; one NULL is
  * FASGD_ERR_NULL.  The events are the caller's (created, and destroyed only
  * after they are recorded or cleared).
  */
