@@ -188,6 +188,32 @@ def fasgd_init_state(theta, n, b, v, last_T, *, lam: int, mu: int = 1, alpha: fl
     return State(st, dict(theta=theta, n=n, b=b, v=v, last_T=last_T))
 
 
+def checkpoint(state: State) -> dict:
+    """The whole server state on the host: the struct's scalars and copies of
+    its arrays (every random draw is keyed by T, so this is all a resumed run
+    needs)."""
+    c = state.c
+    out = {name: getattr(c, name) for name, _ in fasgd_state._fields_
+           if name not in ("theta", "n", "b", "v", "last_T")}
+    out["arrays"] = {k: (t.cpu().clone() if t is not None else None) for k, t in state.tensors.items()}
+    return out
+
+
+def resume_state(ckpt: dict, device="cuda") -> State:
+    """A state rebuilt from checkpoint() into new device arrays; no array is
+    re-initialised (fasgd_init_state would reset n, b, v and last_T)."""
+    import torch
+    tensors = {k: (t.to(device) if t is not None else None) for k, t in ckpt["arrays"].items()}
+    c = fasgd_state()
+    for name, _ in fasgd_state._fields_:
+        if name in ("theta", "n", "b", "v", "last_T"):
+            t = tensors[name]
+            setattr(c, name, _dev_ptr(t, torch.int32 if name == "last_T" else torch.float32, name, True))
+        else:
+            setattr(c, name, ckpt[name])
+    return State(c, tensors)
+
+
 def _dense_args(state: State, grads: Sequence, clients: Sequence[int], grad_ts: Sequence[int]):
     import torch
     K = len(grads)

@@ -257,3 +257,46 @@ def test_push_pass_and_next_selection_prose_reading(mode):
     assert int(B[2].item()) == m and 0 < m < P
     assert torch.equal(A[0][:m], B[0][:m]) and torch.equal(A[3], B[3])
 
+
+
+def test_resume_from_checkpoint_is_bit_exact():
+    """Three pipelined server steps (each a push, 8 gradients and the next
+    push's selection), a checkpoint to the host (the state and the pending
+    push's list), a resume into new device buffers, and two more steps: the
+    same state, T and list, bit for bit, as five steps without the stop
+    (every draw is keyed by T, so the state and T are all a run needs)."""
+    import torch
+    dev = gpu()
+    P, K = 300_007, 8
+    a, b, _, (m_, s_, w), keep = _states(P, dev, fa.MATH_FAST, fa.V_EQUATIONS, seed=41)
+    gs = [to_dev(workload.host_gradient(w, m_, s_, t, seed=41), dev) for t in range(K + 1)]
+    clients, ts = workload.schedule(w, 5 + 6 * (K + 1) + 1)
+
+    def lists():
+        return _select(a, gs[K], 100.0, 5, 1, dev)
+
+    def steps(st, L, n):
+        idx, val, cnt, seg = L
+        ws = fa.allocate_workspace(P, dev)
+        for _ in range(n):
+            T = st.T
+            sl = slice(T + 1, T + 1 + K)
+            fa.fasgd_apply_with_push_and_select(st, idx, val, cnt, seg, clients[T], ts[T], gs[:K], clients[sl],
+                                                ts[sl], gs[K], clients[T + K + 1], 60.0, 1e-8, SEED,
+                                                idx, val, cnt, seg, ws)
+
+    La = lists()
+    Lb = tuple(x.clone() for x in La)
+    steps(a, La, 5)
+    steps(b, Lb, 3)
+    torch.cuda.synchronize()
+    ck = fa.checkpoint(b)
+    ck_lists = tuple(x.cpu() for x in Lb)
+    del b, Lb
+    r = fa.resume_state(ck, dev)
+    Lr = tuple(x.to(dev) for x in ck_lists)
+    steps(r, Lr, 2)
+    _assert_same(a, r)
+    m = int(La[2].item())
+    assert int(Lr[2].item()) == m
+    assert torch.equal(La[0][:m], Lr[0][:m]) and torch.equal(La[3], Lr[3])

@@ -301,3 +301,29 @@ def test_subsample_evolves_like_full_vector():
         oracle.fasgd_apply(sub, g[js], ts[t])
     for name in ("theta", "n", "b", "v", "last_T"):
         np.testing.assert_array_equal(getattr(full, name)[js], getattr(sub, name))
+
+
+def test_oracle_resume_is_exact():
+    """The oracle's state is the whole state: a run split at T0 (state copied
+    and the copy continued) ends where the unsplit run ends, and the
+    selection after it is the same (draws are keyed by T)."""
+    w = workload.WORKLOADS["tiny"]
+    P = 1000
+    theta0, m_, s_ = workload.host_params(w, P)
+    clients, ts = workload.schedule(w, 40)
+    grads = [workload.host_gradient(w, m_, s_, t) for t in range(40)]
+    whole = oracle.init_state(theta0, alpha=0.01)
+    for t in range(40):
+        oracle.fasgd_apply(whole, grads[t], ts[t])
+    first = oracle.init_state(theta0, alpha=0.01)
+    for t in range(17):
+        oracle.fasgd_apply(first, grads[t], ts[t])
+    resumed = first.take(np.arange(P))
+    for t in range(17, 40):
+        oracle.fasgd_apply(resumed, grads[t], ts[t])
+    for name in ("theta", "n", "b", "v", "last_T"):
+        np.testing.assert_array_equal(getattr(resumed, name), getattr(whole, name), err_msg=name)
+    assert resumed.T == whole.T == 40
+    sel_a = oracle.bfasgd_select(whole.v.astype(np.float32), grads[0], 5.0, 1e-8, 3, whole.T, 1)
+    sel_b = oracle.bfasgd_select(resumed.v.astype(np.float32), grads[0], 5.0, 1e-8, 3, resumed.T, 1)
+    assert sel_a[2] == sel_b[2] and np.array_equal(sel_a[0], sel_b[0])
