@@ -532,9 +532,10 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": f"{args.workload}: {w.name}, P={P}, lambda={w.lam}, per step one pass applying "
-                               f"the previous B-FASGD push (~{int(f * 100)}% transmitted) and K={K} FASGD "
-                               f"updates, then the next push's selection; {args.math} math",
+        "config": {"workload": f"{args.workload}: {w.name}, P={P}, lambda={w.lam}, per step one call: a pass "
+                               f"applying the previous B-FASGD push (~{int(f * 100)}% transmitted) and K={K} "
+                               f"FASGD updates and taking the next push's transmit decisions, then that push's "
+                               f"compaction; {args.math} math",
                    "P": P, "K": K, "lambda": w.lam, "math": args.math, "transmit_fraction": f, "c": c},
         "roofline": {"bound": "hbm", "kernel": "fasgd_dense_push_vec", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
