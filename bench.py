@@ -252,7 +252,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print(json.dumps({"error": "this build runs on one GPU: the server update is elementwise and "
+        print(json.dumps({"error": "this library runs on one GPU: the server update is elementwise and "
                                    "would shard by parameter range with no exchange, but no multi-GPU "
                                    "path is built; run with --gpus 1"}), flush=True)
         sys.exit(2)
