@@ -247,7 +247,7 @@ def main():
     ap.add_argument("--workload", default="memscale", choices=["memscale", "large"])
     ap.add_argument("--K", type=int, default=32)
     ap.add_argument("--math", default="fast", choices=["fast", "ieee"])
-    ap.add_argument("--cpu-params", type=int, default=1 << 26,
+    ap.add_argument("--cpu-params", type=int, default=100_000_000,
                     help="parameters in the oracle's CPU-baseline sample (0 = skip)")
     args = ap.parse_args()
 
