@@ -7,8 +7,8 @@
 // counts travel in the kernel arguments, so the host never copies to the
 // device.  Every segment is cut into blocks of kSegSpan parameters:
 //   seg_partial  one fp64 partial sum of v per block, in a fixed order;
-//   seg_decide   one block per segment folds its partials in a fixed order,
-//                divides by the length and decides in fp64;
+//   seg_decide   one block of 1024 threads per segment folds its partials in
+//                a fixed order, divides by the length and decides in fp64;
 //   seg_apply    the FASGD update on the blocks of transmitted segments.
 // Sums are deterministic run to run (fixed assignment and reduction order).
 #include "kernels.hpp"
@@ -32,16 +32,21 @@ __device__ __forceinline__ void block_range(const SegGroup& g, int64_t b, int& i
     hi = lo + kSegSpan < g.start[i + 1] ? lo + kSegSpan : g.start[i + 1];
 }
 
+constexpr int kDecideThreads = 1024;   // one block folds a segment's partials
+constexpr int kDecideAcc = 4;          // independent accumulators per thread
+static_assert(kDecideAcc == 4, "the fold below combines four sums");
+
+template <int THREADS>
 __device__ __forceinline__ double block_sum(double x)
 {
-    __shared__ double wave_sum[kThreads / kWave];
+    __shared__ double wave_sum[THREADS / kWave];
 #pragma unroll
     for (int d = kWave / 2; d > 0; d >>= 1) x += __shfl_xor(x, d, kWave);
     if ((threadIdx.x & (kWave - 1)) == 0) wave_sum[threadIdx.x / kWave] = x;
     __syncthreads();
     double s = 0.0;
 #pragma unroll
-    for (int w = 0; w < kThreads / kWave; ++w) s += wave_sum[w];
+    for (int w = 0; w < THREADS / kWave; ++w) s += wave_sum[w];
     return s;
 }
 
@@ -62,20 +67,28 @@ __global__ __launch_bounds__(kThreads) void seg_partial(const SegGroup g, const 
     } else {
         for (int64_t j = lo + threadIdx.x; j < hi; j += kThreads) acc += static_cast<double>(v[j]);
     }
-    const double s = block_sum(acc);
+    const double s = block_sum<kThreads>(acc);
     if (threadIdx.x == 0) partial[g.partial_base + blockIdx.x] = s;
 }
 
-__global__ __launch_bounds__(kThreads) void seg_decide(const SegGroup g, const double* __restrict__ partial,
+__global__ __launch_bounds__(kDecideThreads) void seg_decide(const SegGroup g, const double* __restrict__ partial,
                                                        float c, float eps_c, uint32_t key0, uint32_t key1,
                                                        uint32_t ctr_T, uint32_t ctr_client,
                                                        uint8_t* __restrict__ transmit)
 {
     const int i = blockIdx.x;
-    double acc = 0.0;
-    for (int64_t b = g.block_prefix[i] + threadIdx.x; b < g.block_prefix[i + 1]; b += kThreads)
-        acc += partial[g.partial_base + b];
-    const double sum = block_sum(acc);
+    // thread t folds partials t, t + 1024, ... into kDecideAcc running sums
+    // (loads of one round issued together), then the sums in a fixed order
+    double acc[kDecideAcc] = {0.0, 0.0, 0.0, 0.0};
+    const int64_t end = g.block_prefix[i + 1];
+    for (int64_t b = g.block_prefix[i] + threadIdx.x; b < end; b += kDecideAcc * kDecideThreads) {
+#pragma unroll
+        for (int q = 0; q < kDecideAcc; ++q) {
+            const int64_t bq = b + q * kDecideThreads;
+            if (bq < end) acc[q] += partial[g.partial_base + bq];
+        }
+    }
+    const double sum = block_sum<kDecideThreads>((acc[0] + acc[1]) + (acc[2] + acc[3]));
     if (threadIdx.x == 0) {
         const int64_t s = g.first_seg + i;
         const double mean = sum / static_cast<double>(g.start[i + 1] - g.start[i]);
@@ -147,7 +160,7 @@ hipError_t launch_seg_decide(const SegGroup& g, const float* v, double* partial,
     seg_partial<<<blocks, kThreads, 0, s>>>(g, v, partial);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    seg_decide<<<static_cast<unsigned>(g.n), kThreads, 0, s>>>(g, partial, c, eps_c, static_cast<uint32_t>(seed),
+    seg_decide<<<static_cast<unsigned>(g.n), kDecideThreads, 0, s>>>(g, partial, c, eps_c, static_cast<uint32_t>(seed),
                                                               static_cast<uint32_t>(seed >> 32), ctr_T, ctr_client,
                                                               transmit);
     return hipGetLastError();
