@@ -10,7 +10,8 @@
  *
  * Conventions shared by every entry point
  *   - Device memory is owned by the caller (allocated e.g. with torch); the
- *     library keeps no pointer beyond a call and allocates nothing.
+ *     library allocates nothing and keeps no pointer beyond a call (the two
+ *     event handles of fasgd_record_next_pass aside, held until used).
  *   - Every call is asynchronous on `stream` (0 = the null stream) and never
  *     synchronises the host.  Results are visible after the stream is
  *     synchronised.
