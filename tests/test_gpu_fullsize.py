@@ -92,9 +92,13 @@ def test_memscale_1e9_step_sampled():
 
 def test_memscale_1e9_fused_step_sampled():
     """The benchmark's step at 1e9 parameters: a K = 32 pass, the push
-    selected at about 10 % with its list index, then one pass applying that
-    push and 32 more gradients (fasgd_apply_with_push), on 4096 sampled
-    parameters against the oracle (near-ties of the fp32 v drift excluded)."""
+    selected at about 10 % with its list index, then the benchmark's call
+    (fasgd_apply_with_push_and_select): one pass applying that push and 32
+    more gradients and taking the next push's decisions, then that push's
+    compaction into the same buffers.  On 4096 sampled parameters: the state
+    against the oracle (near-ties of the fp32 v drift excluded), and the next
+    push's membership and list index against the oracle's decisions from the
+    same fp32 v, exactly."""
     import torch
     dev = gpu()
     w = workload.WORKLOADS["memscale"]
@@ -104,7 +108,7 @@ def test_memscale_1e9_fused_step_sampled():
         pytest.skip(f"needs about 170 GB of free device memory, {free / 1e9:.0f} GB free")
     print(f"memscale fused step: P={P} K={K}", flush=True)
     theta0, m, s = workload.device_params(w, dev)
-    clients, ts = workload.schedule(w, 2 * K + 1)
+    clients, ts = workload.schedule(w, 2 * K + 2)
     js = sample_indices(P, 4096, seed=2)
     jt = torch.from_numpy(js).to(dev)
     st = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, fa.MATH_FAST)
@@ -147,7 +151,9 @@ def test_memscale_1e9_fused_step_sampled():
         assert diff.sum() <= 4
     sel = np.flatnonzero(want & ~diff)
     sl = slice(K + 1, 2 * K + 1)
-    fa.fasgd_apply_with_push(st, idx, val, cnt, seg, clients[K], ts[K], grads[:K], clients[sl], ts[sl])
+    nxt = 2 * K + 1
+    fa.fasgd_apply_with_push_and_select(st, idx, val, cnt, seg, clients[K], ts[K], grads[:K], clients[sl], ts[sl],
+                                        grads[K], clients[nxt], c, 1e-8, SEED, idx, val, cnt, seg, ws)
     oracle.bfasgd_apply_sparse(ref, sel.astype(np.int32), g_host[K][sel], ts[K])
     for k in range(K):
         oracle.fasgd_apply(ref, g_host[k], ts[K + 1 + k])
@@ -156,6 +162,20 @@ def test_memscale_1e9_fused_step_sampled():
     assert_state_close(st, ref.take(keep), RTOL_SEQ, js=torch.from_numpy(js[keep]).to(dev),
                        what="after the pass with the push")
     assert st.T == 2 * K + 1 and st.dense_T == 2 * K
+    # the next push, decided inside the pass from the v it left
+    m2 = int(cnt.item())
+    assert 0.07 < m2 / P < 0.15, m2 / P
+    assert int(seg[-1].item()) == m2
+    starts = seg[torch.from_numpy(segs).to(dev)].long()
+    assert torch.equal(starts, torch.searchsorted(idx[:m2], torch.from_numpy(segs * 256).to(dev).to(torch.int32)))
+    lst = idx[:m2]
+    pos = torch.searchsorted(lst, jt.to(torch.int32))
+    got2 = ((pos < m2) & (lst[pos.clamp(max=m2 - 1)] == jt.to(torch.int32))).cpu().numpy()
+    v_gpu = st.v[jt].cpu().numpy()
+    want2 = oracle.bfasgd_decide(js, v_gpu, c, 1e-8, SEED, st.T, clients[nxt])
+    np.testing.assert_array_equal(got2, want2)
+    vals = val[pos.clamp(max=m2 - 1)].cpu().numpy()
+    np.testing.assert_array_equal(vals[want2].view(np.uint32), g_host[K][want2].view(np.uint32))
     del grads, st, idx, val, ws, seg, lst
     _free()
 
