@@ -300,3 +300,32 @@ def test_resume_from_checkpoint_is_bit_exact():
     m = int(La[2].item())
     assert int(Lr[2].item()) == m
     assert torch.equal(La[0][:m], Lr[0][:m]) and torch.equal(La[3], Lr[3])
+
+
+@pytest.mark.parametrize("c,cap", [(0.0, None), (3e38, None), (60.0, 0)])
+def test_push_pass_and_next_selection_edge_thresholds(c, cap):
+    """The next push at a threshold that sends everything, one that sends
+    nothing, and a capacity of zero (only the count is written): the same
+    count, list and index as the two separate calls."""
+    import torch
+    dev = gpu()
+    P, K = 123_457, 3
+    a, b, _, (m_, s_, w), keep = _states(P, dev, fa.MATH_FAST, fa.V_EQUATIONS, seed=53)
+    g_push = to_dev(workload.host_gradient(w, m_, s_, 5, seed=53), dev)
+    gs = [to_dev(workload.host_gradient(w, m_, s_, 6 + k, seed=53), dev) for k in range(K)]
+    g_next = to_dev(workload.host_gradient(w, m_, s_, 6 + K, seed=53), dev)
+    clients, ts = [k % w.lam for k in range(K)], [6 + k for k in range(K)]
+    idx, val, cnt, seg = _select(a, g_push, 100.0, 5, 1, dev)
+    capacity = P if cap is None else cap
+    A = _selection_buffers(P, capacity, dev)
+    B = _selection_buffers(P, capacity, dev)
+    fa.fasgd_apply_with_push(a, idx, val, cnt, seg, 1, 5, gs, clients, ts)
+    fa.bfasgd_select_compact(a, g_next, c, 1e-8, SEED, a.T, 3, A[0], A[1], A[2], A[4], seg_start=A[3])
+    fa.fasgd_apply_with_push_and_select(b, idx, val, cnt, seg, 1, 5, gs, clients, ts, g_next, 3, c, 1e-8, SEED,
+                                        B[0], B[1], B[2], B[3], B[4])
+    _assert_same(a, b)
+    m = int(A[2].item())
+    assert int(B[2].item()) == m
+    assert m == {0.0: P, 3e38: 0}.get(c, m)
+    u = min(m, capacity)
+    assert torch.equal(A[0][:u], B[0][:u]) and torch.equal(A[3], B[3])
