@@ -19,6 +19,11 @@
 //            an LDS stage at the popcount of the bits before it (ascending
 //            index order), and writes the staged run at group offset + tile
 //            offset in contiguous stores.
+// When the mark step ran inside the preceding dense pass (which leaves the
+// ballot words but no tile counts), the scan counts each tile's ballot bits.
+// Several pushes selected together run as one set of launches with the push
+// as the grid's y index, each with its own gradient, counter words, output
+// slice and workspace slice.
 // The result depends only on (seed, T, client, v, grad), never on timing.
 #include <string.h>
 

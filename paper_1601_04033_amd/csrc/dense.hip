@@ -1,6 +1,8 @@
 // Dense server updates: state initialisation, the K-fused FASGD apply (also
 // with a compacted B-FASGD push applied ahead of the K gradients in the same
-// pass), the K-fused SASGD apply and the synchronous-SGD step.
+// pass, and then optionally with the next push's transmit decisions taken
+// from the v the pass leaves), the K-fused SASGD apply and the
+// synchronous-SGD step.
 //
 // Every update is elementwise and HBM-bound, so the kernels are plain
 // streaming passes: each thread owns 4 consecutive parameters (one 16-byte
