@@ -98,6 +98,80 @@ def cpu_baseline(pool, theta0_host, clients, ts, c, w, K, P_s):
     return (P_s * K + m) / dt, dt, m
 
 
+def large_25m(fa, workload, dev, mode, K=32, reps=20):
+    """The 25M-parameter workload (50 blocks of 500k, lambda = 64) beside the
+    main one: the dense pass at K = 1, 8, 32, the server's step (one
+    fasgd_apply_with_push_and_select call: a 10 % push and K gradients in one
+    pass that also takes the next push's decisions, then its compaction) and
+    the selection on its own, each over calls issued back to back.  Fractions
+    are algorithmic bytes over time against 8 TB/s."""
+    import torch
+    w = workload.WORKLOADS["large"]
+    P = w.P
+    theta0, m, s = workload.device_params(w, dev)
+    pool = [workload.device_gradient(w, m, s, t) for t in range(K + 1)]
+    del m, s
+    theta, n, b, v, last_T = fa.allocate_state(P, dev)
+    theta.copy_(theta0)
+    del theta0
+    st = fa.fasgd_init_state(theta, n, b, v, last_T, lam=w.lam, alpha=w.alpha_fasgd, math_mode=mode)
+    clients, ts = workload.schedule(w, K + 11 * (1 + 8 + 32) + (2 * reps + 4) * (K + 1) + 64)
+    idx = torch.empty(P, device=dev, dtype=torch.int32)
+    val = torch.empty(P, device=dev)
+    cnt = torch.zeros(1, device=dev, dtype=torch.int64)
+    seg = torch.empty(fa.bfasgd_list_index_length(P), device=dev, dtype=torch.int32)
+    ws = fa.allocate_workspace(P, dev)
+    fa.fasgd_apply_updates(st, pool[:K], clients[:K], ts[:K])
+    torch.cuda.synchronize()
+    c = calibrate_c(v, w.transmit_fraction or 0.1)
+
+    def b2b(fn, count):
+        fn()
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(count):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(e) / count
+
+    out = {"P": P, "lambda": w.lam, "dense": {}}
+    for k in (1, 8, 32):
+        def dense(k=k):
+            T = st.T
+            fa.fasgd_apply_updates(st, pool[:k], clients[T:T + k], ts[T:T + k])
+        ms = b2b(dense, 10)
+        out["dense"][f"K={k}"] = {"ms": ms, "frac": P * (32 + 4 * k) / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+    # the server's step, its pass timed alone with events around the kernel
+    T = st.T
+    fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, T, clients[T], idx, val, cnt, ws, seg_start=seg)
+    passes = []
+
+    def step():
+        T = st.T
+        p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        fa.fasgd_record_next_pass(p0, p1)
+        fa.fasgd_apply_with_push_and_select(st, idx, val, cnt, seg, clients[T], ts[T], pool[:K],
+                                            clients[T + 1:T + 1 + K], ts[T + 1:T + 1 + K], pool[K],
+                                            clients[T + K + 1], c, EPS_C, SEED, idx, val, cnt, seg, ws)
+        passes.append((p0, p1))
+    step_ms = b2b(step, reps)
+    torch.cuda.synchronize()
+    pass_ms = sum(a.elapsed_time(e) for a, e in passes[1:]) / len(passes[1:])
+    m = int(cnt.item())
+    pass_bytes = P * (32 + 4 * K) + 8 * m + 4 * fa.bfasgd_list_index_length(P) + P / 8
+    out["step"] = {"ms": step_ms, "param_updates_per_s": (P * K + m) / (step_ms * 1e-3),
+                   "pass_ms": pass_ms, "pass_frac": pass_bytes / (pass_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                   "transmitted_fraction": m / P}
+    T = st.T
+    fa.bfasgd_apply_sparse(st, idx, val, cnt, clients[T], ts[T])
+    sel_ms = b2b(lambda: fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, st.T, clients[st.T], idx, val, cnt,
+                                                  ws), reps)
+    m = int(cnt.item())
+    out["bfasgd_select_compact"] = {"ms": sel_ms, "frac": (8 * P + 8 * m) / (sel_ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+    return out
+
+
 def small_configs(fa, workload, dev, mode, B=16, reps=20):
     """The small workloads, whose state fits the 256 MB Infinity Cache (so
     their GB/s are 'effective', not HBM): the tiny trace (100k parameters,
@@ -518,6 +592,7 @@ def main():
     copy_gbs = 8 * P / (float(np.mean(cp_ms[1:])) * 1e-3) / 1e9
     del anchor
     small = small_configs(fa, workload, dev, mode)
+    large = large_25m(fa, workload, dev, mode) if args.workload != "large" else None
 
     out = {
         "metric": METRIC,
@@ -571,6 +646,7 @@ def main():
                                       "GB/s": 40 * P / (segapply_ms * 1e-3) / 1e9},
             "copy_anchor": {"GB/s": copy_gbs, "bytes": 8 * P},
             "small_configs": small,
+            "large_25m": large,
         },
     }
     if args.cpu_params:
