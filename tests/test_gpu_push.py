@@ -329,3 +329,30 @@ def test_push_pass_and_next_selection_edge_thresholds(c, cap):
     assert m == {0.0: P, 3e38: 0}.get(c, m)
     u = min(m, capacity)
     assert torch.equal(A[0][:u], B[0][:u]) and torch.equal(A[3], B[3])
+
+
+def test_record_next_pass_times_the_pass_once():
+    """The events handed to fasgd_record_next_pass are recorded around the
+    next pass kernel only (inside a call that also selects): the interval is
+    positive and no longer than the whole call, and a later call leaves them
+    alone."""
+    import torch
+    dev = gpu()
+    P, K = 2_000_003, 8
+    a, _, _, (m_, s_, w), keep = _states(P, dev, fa.MATH_FAST, fa.V_EQUATIONS, seed=61)
+    gs = [to_dev(workload.host_gradient(w, m_, s_, 6 + k, seed=61), dev) for k in range(K + 1)]
+    idx, val, cnt, seg = _select(a, gs[K], 100.0, 5, 1, dev)
+    ws = fa.allocate_workspace(P, dev)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    fa.fasgd_record_next_pass(p0, p1)
+    c0.record()
+    fa.fasgd_apply_with_push_and_select(a, idx, val, cnt, seg, 1, 5, gs[:K], list(range(K)), [6 + k for k in range(K)],
+                                        gs[K], 2, 60.0, 1e-8, SEED, idx, val, cnt, seg, ws)
+    c1.record()
+    torch.cuda.synchronize()
+    t_pass, t_call = p0.elapsed_time(p1), c0.elapsed_time(c1)
+    assert 0.0 < t_pass <= t_call
+    fa.fasgd_apply_updates(a, gs[:K], list(range(K)), [a.T + k for k in range(K)])
+    torch.cuda.synchronize()
+    assert p0.elapsed_time(p1) == t_pass
