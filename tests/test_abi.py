@@ -409,3 +409,27 @@ def test_segment_entry_points_reject_bad_arguments(lib):
     assert apply(ts=3) == 3
     assert apply(client=-1) == 4
     assert st.T == 2
+
+
+def test_header_is_c_and_state_layout_matches_binding(tmp_path):
+    """include/fasgd.h compiles as C11, and the binding's ctypes fasgd_state
+    has the C struct's size and field offsets."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    hip_inc = "/opt/rocm/include"
+    if gcc is None or not os.path.isdir(os.path.join(hip_inc, "hip")):
+        pytest.skip("gcc or the HIP headers are not available")
+    fields = [name for name, _ in fa.fasgd_state._fields_]
+    c_names = ["lambda" if n == "lambda_" else n for n in fields]
+    src = tmp_path / "layout.c"
+    src.write_text("#include <stddef.h>\n#include <stdio.h>\n#include \"fasgd.h\"\nint main(void) {\n"
+                   "    printf(\"%zu\\n\", sizeof(fasgd_state));\n" +
+                   "".join(f"    printf(\"%zu\\n\", offsetof(fasgd_state, {n}));\n" for n in c_names) +
+                   "    return 0;\n}\n")
+    exe = tmp_path / "layout"
+    subprocess.run([gcc, "-std=c11", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__", "-I", hip_inc,
+                    "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    got = [int(x) for x in subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split()]
+    want = [ctypes.sizeof(fa.fasgd_state)] + [getattr(fa.fasgd_state, n).offset for n in fields]
+    assert got == want
