@@ -32,7 +32,9 @@ METRIC = "param-updates/sec and achieved HBM GB/s (% of peak), FASGD apply at 25
 HBM_PEAK_GBS = 8000.0
 EPS_C = 1e-8
 SEED = 0x5EED
-PMC_SUMMARY = os.path.join(ROOT, "profiles", "fasgd_dense_push_k32_memscale_1e9_pmc.txt")
+# rocprofv3 counter summaries of the step's pass, per workload
+PMC_SUMMARIES = {"memscale": os.path.join(ROOT, "profiles", "fasgd_dense_push_k32_memscale_1e9_pmc.txt"),
+                 "large": os.path.join(ROOT, "profiles", "fasgd_dense_push_k32_large_25m_pmc.txt")}
 DENSE_SOURCES = [os.path.join(ROOT, "paper_1601_04033_amd", "csrc", f)
                  for f in ("dense.hip", "device_math.hpp", "kernels.hpp")]
 
@@ -50,12 +52,14 @@ def dense_source_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(P, K):
-    """HBM bytes per dense launch from the committed rocprofv3 counter
-    summary, or None when it is absent or the kernel changed since."""
-    if not os.path.exists(PMC_SUMMARY):
+def measured_traffic(workload_name, P, K):
+    """HBM bytes per launch of the step's pass from the committed rocprofv3
+    counter summary of the workload, or None when it is absent, of another
+    shape, or the kernel changed since."""
+    path = PMC_SUMMARIES.get(workload_name)
+    if path is None or not os.path.exists(path):
         return None
-    text = open(PMC_SUMMARY).read()
+    text = open(path).read()
     m_hash = re.search(r"source_hash:\s*([0-9a-f]+)", text)
     m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
     m_shape = re.search(r"shape:\s*P=(\d+)\s+K=(\d+)", text)
@@ -455,7 +459,7 @@ def main():
     # push's decisions (1 bit per parameter)
     pass_bytes = P * (32 + 4 * K) + 8 * m_avg + 4 * fa.bfasgd_list_index_length(P) + P / 8
     achieved = pass_bytes / (pass_ms * 1e-3) / 1e9
-    traffic = measured_traffic(P, K)
+    traffic = measured_traffic(args.workload, P, K)
     sel_ms = float(np.mean(ms["select"]))
     # after the pass took the decisions: ballots and g read, (idx, val) written
     sel_bytes = P * 4 + P / 8 + m_avg * 8
