@@ -4,7 +4,8 @@
 // Work is cut into wave tiles of kTileSegs segments of 64 chunks (one chunk is
 // 4 consecutive parameters, one 16-byte vector).  Every wave owns one tile and
 // never waits on another wave, so no launch has a block barrier in its
-// streaming part.  Selection runs in three or four launches:
+// streaming part.  Selection runs in three or four launches (small calls: two,
+// described at select_mark_wide):
 //   mark     the wave loads its tile of v, draws one Philox4x32-10 call per
 //            chunk (the counter is the global chunk index, so one call feeds
 //            one vector of v), forms four ballots per segment (1 bit per
@@ -100,10 +101,12 @@ __device__ __forceinline__ SelectArgs push_args(const SelectArgs& a0, const Sele
     return a;
 }
 
-// Mark one tile.  FULL: the tile lies inside [0, P) and v is 16-byte
-// aligned, so no lane needs a bounds check (every tile but the last).
-template <bool FULL>
-__device__ __forceinline__ void mark_tile(const SelectArgs& a, int64_t tile, int lane)
+// Mark one tile and return its transmit count (wave-uniform).  FULL: the
+// tile lies inside [0, P) and v is 16-byte aligned, so no lane needs a bounds
+// check (every tile but the last).  STORE_COUNT: also store the count for the
+// scan launch.
+template <bool FULL, bool STORE_COUNT>
+__device__ __forceinline__ uint32_t mark_tile(const SelectArgs& a, int64_t tile, int lane)
 {
     const int64_t nch = n_chunks(a.P);
     const int64_t q0 = tile * kChunksPerTile + lane;
@@ -144,7 +147,8 @@ __device__ __forceinline__ void mark_tile(const SelectArgs& a, int64_t tile, int
     if (lane < kTileWords)
         a.ballots[tile * kTileWords + lane] =
             (static_cast<uint64_t>(static_cast<uint32_t>(word_hi)) << 32) | static_cast<uint32_t>(word_lo);
-    if (lane == 0) a.tile_count[tile] = count;
+    if (STORE_COUNT && lane == 0) a.tile_count[tile] = count;
+    return count;
 }
 
 __global__ __launch_bounds__(kSelBlock) void select_mark(const SelectArgs a0, const SelectBatch bt, bool aligned)
@@ -155,9 +159,9 @@ __global__ __launch_bounds__(kSelBlock) void select_mark(const SelectArgs a0, co
     if (tile >= a.n_tiles) return;
     const int lane = threadIdx.x & (kWave - 1);
     if (aligned && (tile + 1) * kChunksPerTile * 4 <= a.P)
-        mark_tile<true>(a, tile, lane);
+        mark_tile<true, true>(a, tile, lane);
     else
-        mark_tile<false>(a, tile, lane);
+        mark_tile<false, true>(a, tile, lane);
 }
 
 // Block-wide exclusive scan of one value per thread (kScanBlock threads).
@@ -314,15 +318,14 @@ __device__ __forceinline__ void drain(const SelectArgs& a, const int32_t* s_idx,
     }
 }
 
+// Every gradient load of the tile, issued before anything waits on them (at
+// any transmit fraction worth compacting every line holds a transmitted
+// value, so loading the whole tile costs no traffic).
 template <bool FULL>
-__device__ __forceinline__ void scatter_tile(const SelectArgs& a, int64_t tile, int lane, int32_t* s_idx,
-                                             float* s_val)
+__device__ __forceinline__ void load_tile_grad(const SelectArgs& a, int64_t tile, int lane, f4 (&g)[kTileSegs])
 {
     const int64_t nch = n_chunks(a.P);
     const int64_t q0 = tile * kChunksPerTile + lane;
-    // every gradient load of the tile first (at any transmit fraction worth
-    // compacting every line holds a transmitted value, so this costs no traffic)
-    f4 g[kTileSegs];
 #pragma unroll
     for (int s = 0; s < kTileSegs; ++s) {
         const int64_t q = q0 + s * kWave;
@@ -331,9 +334,17 @@ __device__ __forceinline__ void scatter_tile(const SelectArgs& a, int64_t tile, 
         else if (q < nch)
             g[s] = load_chunk(a.grad, q, a.P);
     }
+}
+
+// The tile's entries, with gradients g, to list positions from `base` on.
+// Chunks past P carry no ballot bits, so their (unloaded) gradients are never
+// read.
+__device__ __forceinline__ void scatter_loaded(const SelectArgs& a, int64_t tile, int lane, const f4 (&g)[kTileSegs],
+                                               int64_t base, int32_t* s_idx, float* s_val)
+{
+    const int64_t q0 = tile * kChunksPerTile + lane;
     const uint64_t* tb = a.ballots + tile * kTileWords;
     const uint64_t below = lanes_below(lane);
-    int64_t base = static_cast<int64_t>(a.group_offset[tile / kScanBlock]) + a.tile_offset[tile];
     uint32_t staged = 0;
     uint32_t seg_pos = 0;   // lane s < kTileSegs: list position of segment s's first entry
 #pragma unroll
@@ -374,6 +385,16 @@ __device__ __forceinline__ void scatter_tile(const SelectArgs& a, int64_t tile, 
     }
 }
 
+template <bool FULL>
+__device__ __forceinline__ void scatter_tile(const SelectArgs& a, int64_t tile, int lane, int32_t* s_idx,
+                                             float* s_val)
+{
+    f4 g[kTileSegs];
+    load_tile_grad<FULL>(a, tile, lane, g);
+    const int64_t base = static_cast<int64_t>(a.group_offset[tile / kScanBlock]) + a.tile_offset[tile];
+    scatter_loaded(a, tile, lane, g, base, s_idx, s_val);
+}
+
 __global__ __launch_bounds__(kSelBlock) void select_scatter(const SelectArgs a0, const SelectBatch bt, bool aligned)
 {
     const SelectArgs a = push_args(a0, bt);
@@ -387,6 +408,102 @@ __global__ __launch_bounds__(kSelBlock) void select_scatter(const SelectArgs a0,
         scatter_tile<true>(a, tile, lane, s_idx[w], s_val[w]);
     else
         scatter_tile<false>(a, tile, lane, s_idx[w], s_val[w]);
+}
+
+// Two-launch selection, for calls of at most kMaxWideWork blocks of
+// kWideWaves tiles (all pushes together): no scan launch.  A mark block of
+// kWideWaves waves (one tile each) adds its waves' counts through an LDS
+// arrival counter, so no wave waits for another and there is no global
+// atomic, and the last wave to arrive stores the block total.  Each scatter
+// block covers the same tiles; while its gradient loads are in flight it sums
+// the totals of the blocks before it and, after one block barrier, the counts
+// of its own earlier tiles (from their ballot words), which gives every tile
+// its list position.  The last block writes the count.  Up to about 8M
+// parameters this saves the scan launch's latency (2 of 18 us at 1.8M); past
+// that the block barrier of the scatter costs more than the scan launch.
+constexpr int kWideWaves = 16;
+constexpr int kWideBlock = kWideWaves * kWave;
+constexpr int64_t kMaxWideWork = 512;        // blocks x pushes; block totals live in group_total
+static_assert(kMaxWideWork <= kMaxGroups, "block totals fit the group totals");
+
+__global__ __launch_bounds__(kWideBlock) void select_mark_wide(const SelectArgs a0, const SelectBatch bt,
+                                                               bool aligned)
+{
+    const SelectArgs a = push_args(a0, bt);
+    __shared__ uint32_t s_total, s_arrived;
+    if (threadIdx.x == 0) {
+        s_total = 0;
+        s_arrived = 0;
+    }
+    __syncthreads();
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int64_t tile = static_cast<int64_t>(blockIdx.x) * kWideWaves + w;
+    const int lane = threadIdx.x & (kWave - 1);
+    uint32_t count = 0;
+    if (tile < a.n_tiles) {
+        if (aligned && (tile + 1) * kChunksPerTile * 4 <= a.P)
+            count = mark_tile<true, false>(a, tile, lane);
+        else
+            count = mark_tile<false, false>(a, tile, lane);
+    }
+    if (lane == 0) {
+        __hip_atomic_fetch_add(&s_total, count, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        // release / acquire: every wave's addition is seen by the last to arrive
+        const uint32_t before = __hip_atomic_fetch_add(&s_arrived, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (before == kWideWaves - 1)
+            a.group_total[blockIdx.x] = __hip_atomic_load(&s_total, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+}
+
+__global__ __launch_bounds__(kWideBlock) void select_scatter_wide(const SelectArgs a0, const SelectBatch bt,
+                                                                  bool aligned)
+{
+    const SelectArgs a = push_args(a0, bt);
+    __shared__ int32_t s_idx[kWideWaves][kStageEntries];
+    __shared__ float s_val[kWideWaves][kStageEntries];
+    __shared__ uint32_t s_before[kWideWaves];   // per wave: part of the totals of earlier blocks
+    __shared__ uint32_t s_tile[kWideWaves];     // per wave: its tile's count
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int64_t tile = static_cast<int64_t>(blockIdx.x) * kWideWaves + w;
+    const int lane = threadIdx.x & (kWave - 1);
+    const bool full = aligned && (tile + 1) * kChunksPerTile * 4 <= a.P;
+    f4 g[kTileSegs];
+    if (tile < a.n_tiles) {
+        if (full)
+            load_tile_grad<true>(a, tile, lane, g);
+        else
+            load_tile_grad<false>(a, tile, lane, g);
+    }
+    uint32_t before = 0;
+    for (uint32_t i = threadIdx.x; i < blockIdx.x; i += kWideBlock) before += a.group_total[i];
+#pragma unroll
+    for (int d = kWave / 2; d > 0; d >>= 1) before += __shfl_xor(before, d, kWave);
+    uint32_t mine = 0;
+    if (tile < a.n_tiles) {
+        const uint64_t* tb = a.ballots + tile * kTileWords;
+#pragma unroll
+        for (int k = 0; k < kTileWords; ++k) mine += __popcll(tb[k]);
+    }
+    if (lane == 0) {
+        s_before[w] = before;
+        s_tile[w] = mine;
+    }
+    __syncthreads();
+    int64_t block_base = 0, base = 0;
+#pragma unroll
+    for (int k = 0; k < kWideWaves; ++k) {
+        block_base += s_before[k];
+        if (k < w) base += s_tile[k];
+    }
+    base += block_base;
+    if (tile < a.n_tiles) scatter_loaded(a, tile, lane, g, base, s_idx[w], s_val[w]);
+    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) {
+        int64_t total = block_base;
+#pragma unroll
+        for (int k = 0; k < kWideWaves; ++k) total += s_tile[k];
+        *a.d_count = total;
+        if (a.seg_start) a.seg_start[a.n_segs] = static_cast<uint32_t>(total);
+    }
 }
 
 constexpr int kListBlock = 256;               // list kernels: 4 waves
@@ -479,9 +596,19 @@ hipError_t launch_select(const SelectArgs& a, const SelectBatch& bt, int B, bool
     const unsigned gx = static_cast<unsigned>((a.n_tiles + kWavesPerBlock - 1) / kWavesPerBlock);
     const unsigned groups = static_cast<unsigned>((a.n_tiles + kScanBlock - 1) / kScanBlock);
     if (groups > static_cast<unsigned>(kMaxGroups) || B < 1 || B > kMaxBatch) return hipErrorInvalidValue;
+    const int64_t wide = (a.n_tiles + kWideWaves - 1) / kWideWaves;
+    hipError_t e;
+    if (wide * B <= kMaxWideWork) {
+        const dim3 wgrid(static_cast<unsigned>(wide), static_cast<unsigned>(B));
+        select_mark_wide<<<wgrid, kWideBlock, 0, s>>>(a, bt, aligned);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        select_scatter_wide<<<wgrid, kWideBlock, 0, s>>>(a, bt, aligned);
+        return hipGetLastError();
+    }
     const dim3 grid(gx, static_cast<unsigned>(B));
     select_mark<<<grid, kSelBlock, 0, s>>>(a, bt, aligned);
-    hipError_t e = hipGetLastError();
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (groups <= static_cast<unsigned>(kFusedTopGroups)) {
         select_scan<true, false><<<dim3(groups, B), kScanBlock, 0, s>>>(a, bt);

@@ -71,13 +71,18 @@ def _batch_buffers(B, P, cap, dev):
 @pytest.mark.parametrize("P,B,cap_frac,offset,base", [
     (1, 3, 1.0, 0, 0), (1027, 16, 1.0, 0, 0), (100_003, 16, 1.0, 0, 0), (100_003, 5, 0.05, 0, 0),
     (100_003, 6, 1.0, 0, 4 * 123_457), (1_000_003, 64, 1.0, 0, 0), (65_537, 7, 1.0, 1, 0),
-    (17_000_003, 3, 1.0, 0, 0)])
+    (17_000_003, 3, 1.0, 0, 0), (131_075, 64, 1.0, 0, 0), (4_194_308, 2, 0.5, 0, 0), (4_194_304, 2, 1.0, 1, 0)])
 def test_batch_select_equals_single_selects(P, B, cap_frac, offset, base):
     """Push by push, the batch gives the count, list and list index of a
     single selection with the same gradient, T and client, bit for bit
     (including a capacity cut, a shard offset, the scalar path for gradients
     4 bytes off 16-byte alignment, 64 pushes, and 17M parameters, where the
-    group scan takes its two-launch form)."""
+    group scan takes its two-launch form).  Calls of at most 512 blocks of 16
+    tiles in all take the two-launch selection (block totals, no scan
+    launch), larger ones the scan: at 131,075 x 64 and 4,194,308 x 2 the
+    batch scans while each single push takes the two-launch form, so the two
+    forms are checked against each other; 4,194,304 x 2 is the largest batch
+    of two that takes the two-launch form."""
     import torch
     dev = gpu()
     (st,), _, (m_, s_, w), keep = _mid_run_state(P, dev, seed=P % 977, copies=1)

@@ -83,6 +83,36 @@ def test_select_mlp_twenty_percent_and_deterministic():
         assert m2 == m and np.array_equal(idx2, idx) and np.array_equal(val2, val)
 
 
+@pytest.mark.parametrize("P", [8_388_608, 8_388_612])
+def test_select_at_two_launch_limit(P):
+    """Either side of the largest selection that runs in two launches (512
+    blocks of 16 tiles of 1024 parameters, no scan launch): lists bit-exact
+    against the oracle and the list index pointing at every segment."""
+    import torch
+    dev = gpu()
+    v = workload.synthetic_v(P, seed=5)
+    g = np.random.default_rng(5).standard_normal(P).astype(np.float32)
+    st = _state_with_v(v, dev)
+    idx = torch.full((P,), -7, device=dev, dtype=torch.int32)
+    val = torch.zeros(P, device=dev)
+    cnt = torch.full((1,), -1, device=dev, dtype=torch.int64)
+    seg = torch.full((fa.bfasgd_list_index_length(P),), -1, device=dev, dtype=torch.int32)
+    ws = fa.allocate_workspace(P, dev)
+    ws.fill_(0x5A)
+    fa.bfasgd_select_compact(st, to_dev(g, dev), 40.0, 1e-8, SEED, 77, 5, idx, val, cnt, ws, seg_start=seg)
+    torch.cuda.synchronize()
+    r_idx, r_val, r_m = oracle.bfasgd_select(v, g, 40.0, 1e-8, SEED, 77, 5)
+    m = int(cnt.item())
+    assert m == r_m
+    np.testing.assert_array_equal(idx[:m].cpu().numpy(), r_idx)
+    np.testing.assert_array_equal(val[:m].cpu().numpy().view(np.uint32), r_val.view(np.uint32))
+    assert (idx[m:] == -7).all()
+    want = np.searchsorted(r_idx.astype(np.int64), 256 * np.arange(fa.bfasgd_list_index_length(P) - 1))
+    got = seg.cpu().numpy().astype(np.int64)
+    np.testing.assert_array_equal(got[:-1], want)
+    assert got[-1] == m
+
+
 def test_select_capacity_truncation_and_empty():
     dev = gpu()
     P = 50_000
