@@ -113,6 +113,39 @@ def test_select_at_two_launch_limit(P):
     assert got[-1] == m
 
 
+@pytest.mark.parametrize("P", [workload.MLP_P, 12_000_003])
+def test_select_repeats_bit_identical(P):
+    """100 selections of the same push give the same count, list and list
+    index bit for bit, with the workspace refilled with other bytes between
+    repeats (two launches at the MLP size, the scan form at 12M)."""
+    import torch
+    dev = gpu()
+    v = workload.synthetic_v(P, seed=9)
+    st = _state_with_v(v, dev)
+    g = torch.randn(P, device=dev, generator=torch.Generator(device=dev).manual_seed(9))
+    L = fa.bfasgd_list_index_length(P)
+    idx = torch.empty(P, device=dev, dtype=torch.int32)
+    val = torch.empty(P, device=dev)
+    cnt = torch.zeros(1, device=dev, dtype=torch.int64)
+    seg = torch.empty(L, device=dev, dtype=torch.int32)
+    ws = fa.allocate_workspace(P, dev)
+    fa.bfasgd_select_compact(st, g, 30.0, 1e-8, SEED, 21, 4, idx, val, cnt, ws, seg_start=seg)
+    torch.cuda.synchronize()
+    m = int(cnt.item())
+    first = (idx[:m].clone(), val[:m].clone(), seg.clone())
+    assert 0 < m < P
+    for r in range(100):
+        if r % 10 == 0:
+            ws.fill_((37 * r) % 256)
+            idx.fill_(-1)
+            seg.fill_(-1)
+        fa.bfasgd_select_compact(st, g, 30.0, 1e-8, SEED, 21, 4, idx, val, cnt, ws, seg_start=seg)
+        assert torch.equal(cnt, torch.tensor([m], device=dev)), r
+        assert torch.equal(idx[:m], first[0]), r
+        assert torch.equal(val[:m].view(torch.int32), first[1].view(torch.int32)), r
+        assert torch.equal(seg, first[2]), r
+
+
 def test_select_capacity_truncation_and_empty():
     dev = gpu()
     P = 50_000
