@@ -52,10 +52,13 @@ def dense_source_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload_name, P, K):
+def measured_traffic(workload_name, P, K, math="fast"):
     """HBM bytes per launch of the step's pass from the committed rocprofv3
     counter summary of the workload, or None when it is absent, of another
-    shape, or the kernel changed since."""
+    shape or math mode (the counters were taken in fast math), or the kernel
+    changed since."""
+    if math != "fast":
+        return None
     path = PMC_SUMMARIES.get(workload_name)
     if path is None or not os.path.exists(path):
         return None
@@ -459,7 +462,7 @@ def main():
     # push's decisions (1 bit per parameter)
     pass_bytes = P * (32 + 4 * K) + 8 * m_avg + 4 * fa.bfasgd_list_index_length(P) + P / 8
     achieved = pass_bytes / (pass_ms * 1e-3) / 1e9
-    traffic = measured_traffic(args.workload, P, K)
+    traffic = measured_traffic(args.workload, P, K, args.math)
     sel_ms = float(np.mean(ms["select"]))
     # after the pass took the decisions: ballots and g read, (idx, val) written
     sel_bytes = P * 4 + P / 8 + m_avg * 8

@@ -32,6 +32,7 @@ def test_traffic_only_for_its_own_shape(name):
     assert bench.measured_traffic(name, P, K + 1) is None
     assert bench.measured_traffic(name, P + 1, K) is None
     assert bench.measured_traffic("mlp", P, K) is None
+    assert bench.measured_traffic(name, P, K, math="ieee") is None
     got = bench.measured_traffic(name, P, K)
     text = open(bench.PMC_SUMMARIES[name]).read()
     if f"source_hash: {bench.dense_source_hash()}" in text:
