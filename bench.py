@@ -396,11 +396,9 @@ def main():
 
     def step(i, timed, c):
         base = st.T                          # the schedule is indexed by server timestamp
-        e0 = torch.cuda.Event(enable_timing=True)
         p0 = torch.cuda.Event(enable_timing=True)
         p1 = torch.cuda.Event(enable_timing=True)
         e2 = torch.cuda.Event(enable_timing=True)
-        e0.record()
         out_cnt = cnts[i + 1:i + 2]
         if pending:
             pc, pts, j = pending.pop()
