@@ -1,0 +1,189 @@
+"""Seeded random parity sweep through the C ABI: configurations drawn from a
+fixed seed per case (sizes with ragged tails and sizes next to the vector,
+segment and tile edges; thresholds, keys, shard offsets, capacity cuts and
+misaligned views; both math modes and both readings of v; random K and
+staleness), each held to the same bar as the enumerated tests:
+ * the selection against the oracle, bit-exact, with the list index;
+ * a K-update sequence against the oracle within the sequence tolerance;
+ * the push applied inside the pass, and the server's step that also takes
+   the next push's decisions, bit-identical to the separate calls."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1601_04033_amd as fa
+import workload
+from helpers import RTOL_SEQ, assert_state_close, gpu, new_gpu_state, to_dev
+
+pytestmark = pytest.mark.gpu
+N_CASES = 48
+EDGES = (4, 256, 1024, 4096, 16384, 65536, 262144)
+
+
+def _size(rng, hi):
+    kind = rng.integers(0, 3)
+    if kind == 0:
+        return int(rng.integers(1, 300))
+    if kind == 1:
+        e = int(rng.choice(EDGES)) * int(rng.integers(1, 9))
+        return int(min(max(1, e + int(rng.integers(-5, 6))), hi))
+    return int(np.exp(rng.uniform(np.log(300), np.log(hi))))
+
+
+def _offset_view(host, dev, off):
+    """A device copy of host starting `off` floats into its buffer."""
+    import torch
+    buf = torch.empty(host.shape[0] + off, device=dev, dtype=torch.float32)
+    buf[off:].copy_(torch.from_numpy(host))
+    return buf[off:]
+
+
+@pytest.mark.parametrize("case", range(N_CASES))
+def test_random_selection_matches_oracle(case):
+    import torch
+    rng = np.random.default_rng(1000 + case)
+    dev = gpu()
+    P = _size(rng, 3_000_000)
+    v = workload.synthetic_v(P, seed=case, lo=float(rng.uniform(0.1, 10)), hi=float(rng.uniform(20, 400)))
+    g = rng.standard_normal(P).astype(np.float32)
+    c = float(np.float32(np.exp(rng.uniform(np.log(0.05), np.log(5e3)))))
+    eps_c = float(rng.choice([0.0, 1e-8, 1e-3]))
+    seed = int(rng.integers(0, 2 ** 63))
+    T = int(rng.integers(0, 2 ** 32))
+    lam = int(rng.integers(1, 300))
+    client = int(rng.integers(0, lam))
+    base = 4 * int(rng.integers(0, 2 ** 40)) if rng.random() < 0.5 else 0
+    v_off, g_off = int(rng.random() < 0.25), int(rng.random() < 0.25)
+    r_idx, r_val, r_m = oracle.bfasgd_select(v, g, c, eps_c, seed, T, client, index_base=base)
+    cap = P if rng.random() < 0.7 else int(rng.integers(0, r_m + 2))
+    print(f"case {case}: P={P} c={c:.4g} eps_c={eps_c} base={base} offsets={v_off},{g_off} cap={cap} m={r_m}",
+          flush=True)
+
+    st = new_gpu_state(np.zeros(P, np.float32), dev, lam, 0.005, fa.MATH_FAST)
+    vd = _offset_view(v, dev, v_off)
+    st.c.v = vd.data_ptr()
+    st.tensors["v"] = vd
+    st.c.index_base = base
+    gd = _offset_view(g, dev, g_off)
+    idx = torch.full((max(cap, 1),), -7, device=dev, dtype=torch.int32)[:cap]
+    val = torch.zeros(max(cap, 1), device=dev)[:cap]
+    cnt = torch.full((1,), -1, device=dev, dtype=torch.int64)
+    seg = torch.full((fa.bfasgd_list_index_length(P),), -1, device=dev, dtype=torch.int32)
+    ws = fa.allocate_workspace(P, dev)
+    ws.fill_(int(rng.integers(0, 256)))
+    fa.bfasgd_select_compact(st, gd, c, eps_c, seed, T, client, idx, val, cnt, ws, seg_start=seg)
+    torch.cuda.synchronize()
+    m = int(cnt.item())
+    assert m == r_m
+    u = min(m, cap)
+    np.testing.assert_array_equal(idx[:u].cpu().numpy(), r_idx[:u])
+    np.testing.assert_array_equal(val[:u].cpu().numpy().view(np.uint32), r_val[:u].view(np.uint32))
+    assert (idx[u:] == -7).all()
+    want = np.searchsorted(r_idx.astype(np.int64), 256 * np.arange(fa.bfasgd_list_index_length(P) - 1))
+    got = seg.cpu().numpy().astype(np.int64)
+    np.testing.assert_array_equal(got[:-1], want)
+    assert got[-1] == m
+
+
+@pytest.mark.parametrize("case", range(N_CASES))
+def test_random_dense_sequence_matches_oracle(case):
+    rng = np.random.default_rng(2000 + case)
+    dev = gpu()
+    P = _size(rng, 400_000)
+    mode = int(rng.choice([fa.MATH_FAST, fa.MATH_IEEE]))
+    reading = int(rng.choice([fa.V_EQUATIONS, fa.V_PROSE]))
+    lam = int(rng.integers(1, 65))
+    gamma, beta = float(rng.uniform(0.5, 0.999)), float(rng.uniform(0.5, 0.999))
+    eps = float(10 ** rng.uniform(-6, -2))
+    alpha = float(10 ** rng.uniform(-4, -1.5))
+    theta0 = rng.normal(0.0, 0.05, P).astype(np.float32)
+    sd = float(10 ** rng.uniform(-3, 0))
+    print(f"case {case}: P={P} mode={mode} reading={reading} lam={lam} gamma={gamma:.4f} beta={beta:.4f} "
+          f"eps={eps:.3g} alpha={alpha:.3g} sd={sd:.3g}", flush=True)
+    st = new_gpu_state(theta0, dev, lam, alpha, mode, gamma=gamma, beta=beta, eps=eps, v_reading=reading)
+    ref = oracle.init_state(theta0, alpha=alpha, gamma=gamma, beta=beta, eps=eps, v_reading=reading)
+    left = 64
+    while left > 0:
+        K = int(rng.integers(1, left + 1))
+        left -= K
+        grads = [(sd * rng.standard_normal(P)).astype(np.float32) for _ in range(K)]
+        clients = [int(x) for x in rng.integers(0, lam, K)]
+        ts = []
+        for k in range(K):
+            Tk = st.T + k
+            ts.append(Tk - min(Tk, int(rng.integers(0, 2 * lam + 1))))
+        fa.fasgd_apply_updates(st, [to_dev(x, dev) for x in grads], clients, ts)
+        for k in range(K):
+            oracle.fasgd_apply(ref, grads[k], ts[k])
+    assert_state_close(st, ref, RTOL_SEQ, what=f"case {case}")
+
+
+def _two_states(P, dev, rng, mode, reading, off):
+    """Two identical mid-run GPU states (random n, b, v, theta; T = 9)."""
+    import torch
+    theta0 = rng.normal(0.0, 0.05, P).astype(np.float32)
+    b0 = (1e-3 * rng.standard_normal(P)).astype(np.float32)
+    n0 = (b0 * b0 + np.float32(1e-4) * rng.random(P).astype(np.float32)).astype(np.float32)
+    v0 = workload.synthetic_v(P, seed=int(rng.integers(0, 1000)), lo=5.0, hi=100.0)
+    out = []
+    for _ in range(2):
+        bufs = fa.allocate_state(P + off, dev)
+        theta, n, b, v, last_T = (t[off:] for t in bufs)
+        st = fa.fasgd_init_state(theta, n, b, v, last_T, lam=32, alpha=0.005, math_mode=mode, v_reading=reading)
+        for t, a in ((theta, theta0), (n, n0), (b, b0), (v, v0)):
+            t.copy_(torch.from_numpy(a))
+        st.c.T = 9
+        out.append((st, bufs))
+    return out
+
+
+@pytest.mark.parametrize("case", range(N_CASES))
+def test_random_push_pass_and_step_are_bit_identical(case):
+    import torch
+    rng = np.random.default_rng(3000 + case)
+    dev = gpu()
+    P = _size(rng, 2_000_000)
+    mode = int(rng.choice([fa.MATH_FAST, fa.MATH_IEEE]))
+    reading = int(rng.choice([fa.V_EQUATIONS, fa.V_PROSE]))
+    off = int(rng.random() < 0.25)
+    K = int(rng.integers(1, 65))
+    c1, c2 = (float(np.float32(np.exp(rng.uniform(np.log(1.0), np.log(2e3))))) for _ in range(2))
+    seed = int(rng.integers(0, 2 ** 63))
+    print(f"case {case}: P={P} mode={mode} reading={reading} offset={off} K={K} c={c1:.4g},{c2:.4g}", flush=True)
+    (a, keep_a), (b, keep_b) = _two_states(P, dev, rng, mode, reading, off)
+    g_push = to_dev(rng.standard_normal(P).astype(np.float32), dev)
+    gs = [to_dev((1e-2 * rng.standard_normal(P)).astype(np.float32), dev) for _ in range(K)]
+    g_next = to_dev(rng.standard_normal(P).astype(np.float32), dev)
+    clients = [int(x) for x in rng.integers(0, 32, K)]
+    ts = [10 + k - int(rng.integers(0, 10)) for k in range(K)]
+    pc, pts = int(rng.integers(0, 32)), 9 - int(rng.integers(0, 9))
+    next_client = int(rng.integers(0, 32))
+    L = fa.bfasgd_list_index_length(P)
+
+    def lists():
+        return (torch.full((P,), -1, device=dev, dtype=torch.int32), torch.zeros(P, device=dev),
+                torch.zeros(1, device=dev, dtype=torch.int64), torch.full((L,), -1, device=dev, dtype=torch.int32))
+
+    idx, val, cnt, seg = lists()
+    fa.bfasgd_select_compact(a, g_push, c1, 1e-8, seed, 9, pc, idx, val, cnt, fa.allocate_workspace(P, dev),
+                             seg_start=seg)
+    # separate calls on a: the push, the K gradients, then the next push's selection
+    fa.bfasgd_apply_sparse(a, idx, val, cnt, pc, pts)
+    fa.fasgd_apply_updates(a, gs, clients, ts)
+    n_idx, n_val, n_cnt, n_seg = lists()
+    fa.bfasgd_select_compact(a, g_next, c2, 1e-8, seed, a.T, next_client, n_idx, n_val, n_cnt,
+                             fa.allocate_workspace(P, dev), seg_start=n_seg)
+    # the server's step on b: one call
+    o_idx, o_val, o_cnt, o_seg = lists()
+    fa.fasgd_apply_with_push_and_select(b, idx, val, cnt, seg, pc, pts, gs, clients, ts, g_next, next_client,
+                                        c2, 1e-8, seed, o_idx, o_val, o_cnt, o_seg, fa.allocate_workspace(P, dev))
+    torch.cuda.synchronize()
+    for name in ("theta", "n", "b", "v"):
+        assert torch.equal(a.tensors[name], b.tensors[name]), name
+    assert a.T == b.T
+    assert torch.equal(a.last_update(), b.last_update())
+    m = int(n_cnt.item())
+    assert int(o_cnt.item()) == m
+    assert torch.equal(o_idx[:m], n_idx[:m])
+    assert torch.equal(o_val[:m].view(torch.int32), n_val[:m].view(torch.int32))
+    assert torch.equal(o_seg, n_seg)
