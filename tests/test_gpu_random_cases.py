@@ -6,7 +6,9 @@ staleness), each held to the same bar as the enumerated tests:
  * the selection against the oracle, bit-exact, with the list index;
  * a K-update sequence against the oracle within the sequence tolerance;
  * the push applied inside the pass, and the server's step that also takes
-   the next push's decisions, bit-identical to the separate calls."""
+   the next push's decisions, bit-identical to the separate calls;
+ * a batch of pushes, selected and applied together, bit-identical to the
+   single calls."""
 import numpy as np
 import pytest
 
@@ -187,3 +189,62 @@ def test_random_push_pass_and_step_are_bit_identical(case):
     assert torch.equal(o_idx[:m], n_idx[:m])
     assert torch.equal(o_val[:m].view(torch.int32), n_val[:m].view(torch.int32))
     assert torch.equal(o_seg, n_seg)
+
+
+@pytest.mark.parametrize("case", range(N_CASES))
+def test_random_batches_equal_single_calls(case):
+    """A batch of B pushes: the batched selection equals B single selections
+    (count, list, list index) and the batched apply equals B sparse applies
+    in order (theta, n, b, v, last_T, T), bit for bit."""
+    import torch
+    rng = np.random.default_rng(4000 + case)
+    dev = gpu()
+    P = _size(rng, 1_000_000)
+    B = int(rng.integers(1, 65))
+    while B > 1 and B * P > 16_000_000:
+        B //= 2
+    mode = int(rng.choice([fa.MATH_FAST, fa.MATH_IEEE]))
+    reading = int(rng.choice([fa.V_EQUATIONS, fa.V_PROSE]))
+    off = int(rng.random() < 0.25)
+    c = float(rng.choice([0.0, 3e38, float(np.float32(np.exp(rng.uniform(np.log(0.05), np.log(5e3)))))],
+                         p=[0.1, 0.1, 0.8]))
+    eps_c = float(rng.choice([0.0, 1e-8]))
+    seed = int(rng.integers(0, 2 ** 63))
+    cap = P if rng.random() < 0.7 else int(rng.integers(0, P // 4 + 2))
+    print(f"case {case}: P={P} B={B} mode={mode} reading={reading} offset={off} c={c:.4g} cap={cap}", flush=True)
+    (a, keep_a), (b, keep_b) = _two_states(P, dev, rng, mode, reading, off)
+    grads = [to_dev(rng.standard_normal(P).astype(np.float32), dev) for _ in range(B)]
+    Ts = [9 + k for k in range(B)]
+    clients = [int(x) for x in rng.integers(0, 32, B)]
+    grad_ts = [9 + k - int(rng.integers(0, 10 + k)) for k in range(B)]
+    L = fa.bfasgd_list_index_length(P)
+    idx = torch.full((B, max(cap, 1)), -1, device=dev, dtype=torch.int32)[:, :cap]
+    val = torch.zeros((B, max(cap, 1)), device=dev)[:, :cap]
+    cnt = torch.zeros(B, device=dev, dtype=torch.int64)
+    seg = torch.full((B, L), -1, device=dev, dtype=torch.int32)
+    ws = torch.empty(B * fa.bfasgd_workspace_bytes(P), device=dev, dtype=torch.uint8)
+    if cap == 0:
+        idx = torch.empty((B, 0), device=dev, dtype=torch.int32)
+        val = torch.empty((B, 0), device=dev)
+    fa.bfasgd_select_compact_batch(a, grads, c, eps_c, seed, Ts, clients, idx, val, cnt, ws, seg_start=seg)
+    ws1 = fa.allocate_workspace(P, dev)
+    for k in range(B):
+        i1 = torch.full((max(cap, 1),), -1, device=dev, dtype=torch.int32)[:cap]
+        v1 = torch.zeros(max(cap, 1), device=dev)[:cap]
+        c1 = torch.zeros(1, device=dev, dtype=torch.int64)
+        s1 = torch.full((L,), -1, device=dev, dtype=torch.int32)
+        fa.bfasgd_select_compact(a, grads[k], c, eps_c, seed, Ts[k], clients[k], i1, v1, c1, ws1, seg_start=s1)
+        torch.cuda.synchronize()
+        m = int(c1.item())
+        assert int(cnt[k].item()) == m, k
+        u = min(m, cap)
+        assert torch.equal(idx[k, :u], i1[:u]), k
+        assert torch.equal(val[k, :u].view(torch.int32), v1[:u].view(torch.int32)), k
+        assert torch.equal(seg[k], s1), k
+    for k in range(B):
+        fa.bfasgd_apply_sparse(a, idx[k], val[k], cnt[k:k + 1], clients[k], grad_ts[k])
+    fa.fasgd_apply_pushes(b, idx, val, cnt, seg, clients, grad_ts)
+    torch.cuda.synchronize()
+    for name in ("theta", "n", "b", "v", "last_T"):
+        assert torch.equal(a.tensors[name].view(torch.int32), b.tensors[name].view(torch.int32)), name
+    assert a.T == b.T == 9 + B and a.dense_T == b.dense_T
