@@ -8,14 +8,16 @@ staleness), each held to the same bar as the enumerated tests:
  * the push applied inside the pass, and the server's step that also takes
    the next push's decisions, bit-identical to the separate calls;
  * a batch of pushes, selected and applied together, bit-identical to the
-   single calls."""
+   single calls;
+ * the widened paths: a synchronous SGD step, per-segment decisions and the
+   segment apply, a cached push and a fetch refresh, against the oracle."""
 import numpy as np
 import pytest
 
 import oracle
 import paper_1601_04033_amd as fa
 import workload
-from helpers import RTOL_SEQ, assert_state_close, gpu, new_gpu_state, to_dev
+from helpers import RTOL_ONE, RTOL_SEQ, assert_close, assert_state_close, gpu, new_gpu_state, to_dev
 
 pytestmark = pytest.mark.gpu
 N_CASES = 48
@@ -248,3 +250,96 @@ def test_random_batches_equal_single_calls(case):
     for name in ("theta", "n", "b", "v", "last_T"):
         assert torch.equal(a.tensors[name].view(torch.int32), b.tensors[name].view(torch.int32)), name
     assert a.T == b.T == 9 + B and a.dense_T == b.dense_T
+
+
+def _near_tie(got, want, mean, c, eps_c, seed, T, client):
+    """Segment decisions equal, except where r lies within 1e-12 of the fp64
+    threshold (the two sides sum v in different orders)."""
+    for s in np.flatnonzero(got != want):
+        w = oracle.philox4x32_10([s & 0xFFFFFFFF, 0x80000000 | (s >> 32), T & 0xFFFFFFFF, client],
+                                 [seed & 0xFFFFFFFF, seed >> 32])[0]
+        t = mean[s] + float(np.float32(eps_c))
+        p = t / (t + c)
+        assert abs((int(w) >> 8) * 2.0 ** -24 - p) <= 1e-12 * p, (s, got[s], want[s])
+
+
+@pytest.mark.parametrize("case", range(N_CASES))
+def test_random_widened_paths_match_oracle(case):
+    """The widened server paths on random sizes and settings: a synchronous
+    SGD step, per-segment decisions and the segment apply, a push with its
+    dropped values taken from the client's cache, and a fetch refresh."""
+    import torch
+    rng = np.random.default_rng(5000 + case)
+    dev = gpu()
+    P = _size(rng, 300_000)
+    lam = int(rng.integers(1, 40))
+    mode = int(rng.choice([fa.MATH_FAST, fa.MATH_IEEE]))
+    reading = int(rng.choice([fa.V_EQUATIONS, fa.V_PROSE]))
+    seed = int(rng.integers(0, 2 ** 63))
+    print(f"case {case}: P={P} lam={lam} mode={mode} reading={reading}", flush=True)
+    theta0 = rng.normal(0.0, 0.05, P).astype(np.float32)
+
+    # synchronous SGD: lambda gradients, one step
+    st = new_gpu_state(theta0, dev, lam, 0.04, fa.MATH_FAST, sasgd=True)
+    ref = oracle.init_state(theta0, alpha=0.04)
+    lr = float(10 ** rng.uniform(-3, -1))
+    grads = [(0.1 * rng.standard_normal(P)).astype(np.float32) for _ in range(lam)]
+    fa.sgd_sync_apply(st, [to_dev(g, dev) for g in grads], lr)
+    oracle.sync_sgd_apply(ref, grads, lr)
+    torch.cuda.synchronize()
+    assert_close(st.theta.cpu().numpy(), ref.theta, RTOL_ONE, what="sync step")
+    assert st.T == ref.T == 1
+
+    # a FASGD state after a few dense updates, then per-segment pushes, a
+    # cached push and a fetch
+    st = new_gpu_state(theta0, dev, lam, 0.005, mode, v_reading=reading)
+    ref = oracle.init_state(theta0, alpha=0.005, v_reading=reading)
+    for t in range(3):
+        g = (0.01 * rng.standard_normal(P)).astype(np.float32)
+        fa.fasgd_apply_updates(st, [to_dev(g, dev)], [t % lam], [t])
+        oracle.fasgd_apply(ref, g, t)
+    S = int(rng.integers(1, min(P, 50) + 1))
+    seg = np.unique(np.concatenate([[0, P], rng.integers(1, P, S - 1) if P > 1 else []])).astype(np.int64)
+    S = seg.size - 1
+    c = float(np.float32(np.exp(rng.uniform(np.log(0.1), np.log(1e3)))))
+    T, client = st.T, int(rng.integers(0, lam))
+    d = torch.zeros(S, device=dev, dtype=torch.uint8)
+    ws = torch.empty(fa.bfasgd_segments_workspace_bytes(P, S), device=dev, dtype=torch.uint8)
+    fa.bfasgd_decide_segments(st, seg, c, 1e-8, seed, T, client, d, ws)
+    torch.cuda.synchronize()
+    got = d.cpu().numpy().astype(bool)
+    v32 = st.v.cpu().numpy()
+    want, mean = oracle.bfasgd_decide_segments(v32, seg, c, 1e-8, seed, T, client)
+    _near_tie(got, want, mean, c, 1e-8, seed, T, client)
+    g = (0.01 * rng.standard_normal(P)).astype(np.float32)
+    fa.bfasgd_apply_segments(st, to_dev(g, dev), seg, d, client, T - 1)
+    oracle.bfasgd_apply_segments(ref, g, seg, got.astype(np.uint8), T - 1)
+    torch.cuda.synchronize()
+    assert_state_close(st, ref, RTOL_SEQ, what="after the segment push")
+
+    cl = int(rng.integers(0, lam))
+    cache_h = (0.01 * rng.standard_normal(P)).astype(np.float32)
+    cache_d = to_dev(cache_h, dev)
+    g = (0.01 * rng.standard_normal(P)).astype(np.float32)
+    idx, val, mm = oracle.bfasgd_select(st.v.cpu().numpy(), g, c, 1e-8, seed, st.T, cl)
+    cnt = torch.full((1,), mm, device=dev, dtype=torch.int64)
+    fa.bfasgd_apply_cached(st, to_dev(idx, dev) if mm else torch.zeros(1, device=dev, dtype=torch.int32),
+                           to_dev(val, dev) if mm else torch.zeros(1, device=dev), cnt, cache_d, cl, st.T - 1)
+    oracle.bfasgd_apply_cached(ref, cache_h, idx, val, ref.T - 1)
+    torch.cuda.synchronize()
+    assert_state_close(st, ref, RTOL_SEQ, what="after the cached push")
+    np.testing.assert_array_equal(cache_d.cpu().numpy().view(np.uint32), cache_h.view(np.uint32))
+
+    copy_h = rng.standard_normal(P).astype(np.float32)
+    copy_d = to_dev(copy_h, dev)
+    theta_now = st.theta.cpu().numpy()
+    fi, fv, fm = oracle.bfasgd_select(st.v.cpu().numpy(), theta_now, c, 1e-8, seed ^ 1, st.T, cl)
+    i_d = torch.empty(P, device=dev, dtype=torch.int32)
+    v_d = torch.empty(P, device=dev)
+    c_d = torch.zeros(1, device=dev, dtype=torch.int64)
+    fa.bfasgd_select_compact(st, st.theta, c, 1e-8, seed ^ 1, st.T, cl, i_d, v_d, c_d, fa.allocate_workspace(P, dev))
+    fa.bfasgd_apply_fetch(copy_d, i_d, v_d, c_d)
+    torch.cuda.synchronize()
+    assert int(c_d.item()) == fm
+    copy_h[fi] = fv
+    np.testing.assert_array_equal(copy_d.cpu().numpy().view(np.uint32), copy_h.view(np.uint32))
