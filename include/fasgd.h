@@ -21,7 +21,8 @@
  *   - Device arrays are plain, densely packed 1-D arrays of P elements in
  *     parameter order (structure of arrays).  4-byte alignment is required;
  *     16-byte alignment of every array (as torch allocations have) selects
- *     the vectorised kernels.
+ *     the vectorised kernels.  Without it the kernels take one parameter
+ *     per thread and P is limited to 2^32 - 256 (FASGD_ERR_ALIGN beyond).
  *   - Calls that share a state must be issued on one stream (or otherwise
  *     ordered by the caller); concurrent calls on one state race.
  */

@@ -60,12 +60,13 @@ __global__ __launch_bounds__(kBlock) void init_kernel(float* __restrict__ n, flo
                                                       float* __restrict__ v, int32_t* __restrict__ last_T,
                                                       int64_t P, float n0, float b0, float v0)
 {
-    const int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-    if (j >= P) return;
-    if (n) n[j] = n0;
-    if (b) b[j] = b0;
-    if (v) v[j] = v0;
-    last_T[j] = -1;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; j < P; j += stride) {
+        if (n) n[j] = n0;
+        if (b) b[j] = b0;
+        if (v) v[j] = v0;
+        last_T[j] = -1;
+    }
 }
 
 // K-fused FASGD over 16-byte aligned arrays; thread i owns parameters
@@ -424,7 +425,7 @@ __global__ __launch_bounds__(kBlock) void sync_sgd_scalar(const DenseArgs a)
 hipError_t launch_init(float* n, float* b, float* v, int32_t* last_T, int64_t P,
                        float n0, float b0, float v0, hipStream_t s)
 {
-    init_kernel<<<grid_for(P), kBlock, 0, s>>>(n, b, v, last_T, P, n0, b0, v0);
+    init_kernel<<<grid_for(P < kMaxScalarItems ? P : kMaxScalarItems), kBlock, 0, s>>>(n, b, v, last_T, P, n0, b0, v0);
     return hipGetLastError();
 }
 
@@ -467,8 +468,10 @@ hipError_t launch_fasgd_dense_push(const DenseArgs& a, const PushArgs& p, const 
 hipError_t launch_fasgd_dense(const DenseArgs& a, int variant, bool aligned, hipStream_t s)
 {
     // vector path (nvec chunks plus one thread for the tail) for K > 1 over
-    // 16-byte aligned arrays; one parameter per thread otherwise
-    const bool vec = aligned && a.K > 1;
+    // 16-byte aligned arrays, and for any K beyond the one-per-thread limit;
+    // one parameter per thread otherwise
+    const bool vec = aligned && (a.K > 1 || a.P > kMaxScalarItems);
+    if (!vec && a.P > kMaxScalarItems) return hipErrorInvalidValue;   // the API rejects this first
     const unsigned grid = vec ? grid_for((a.P >> 2) + 1) : grid_for(a.P);
     switch (variant) {
     case kernel_variant(MATH_FAST, 0): launch_dense_variant<kernel_variant(MATH_FAST, 0)>(a, vec, grid, s); break;

@@ -75,6 +75,16 @@ fasgd_status check_state(const fasgd_state* st, bool need_stats)
     return FASGD_OK;
 }
 
+// Arrays that are not all 16-byte aligned take the one-parameter-per-thread
+// kernels, whose launches cover fewer than 2^32 parameters.
+fasgd_status scalar_size_ok(int64_t P, bool vec)
+{
+    if (!vec && P > fasgd::kMaxScalarItems)
+        return fail(FASGD_ERR_ALIGN, "P = %lld needs 16-byte aligned arrays (at most %lld otherwise)", (long long)P,
+                    (long long)fasgd::kMaxScalarItems);
+    return FASGD_OK;
+}
+
 // kernel template variant of a validated state
 int variant_of(const fasgd_state* st)
 {
@@ -132,6 +142,8 @@ fasgd_status dense_common(fasgd_state* st, const float* const* grads, const int3
         const bool rate = !fasgd_mode || st->math_mode == FASGD_MATH_FAST;
         a.coef[k] = rate ? st->alpha / tau_div[k] : tau_div[k];
     }
+    s = scalar_size_ok(st->P, vec);
+    if (s != FASGD_OK) return s;
     a.theta = st->theta;
     a.n = st->n;
     a.b = st->b;
@@ -567,6 +579,8 @@ fasgd_status sgd_sync_apply(fasgd_state* st, const float* const* grads, float lr
         if (!aligned(grads[k], 4)) return fail(FASGD_ERR_ALIGN, "grads[%d] is not 4-byte aligned", k);
         vec = vec && aligned(grads[k], 16);
     }
+    s = scalar_size_ok(st->P, vec);
+    if (s != FASGD_OK) return s;
     // lambda gradients in passes of at most FASGD_MAX_K; theta is stored in
     // fp32 between passes exactly as it is held in registers within one
     for (int32_t k0 = 0; k0 < st->lambda; k0 += FASGD_MAX_K) {
@@ -603,6 +617,10 @@ fasgd_status bfasgd_apply_cached(fasgd_state* st, const int32_t* idx, const floa
     float tau_div;
     s = staleness(st, &client, &grad_ts, 1, &tau_div);
     if (s != FASGD_OK) return s;
+    const bool vec = aligned(st->theta, 16) && aligned(st->n, 16) && aligned(st->b, 16) && aligned(st->v, 16) &&
+                     aligned(cache, 16);
+    s = scalar_size_ok(st->P, vec);
+    if (s != FASGD_OK) return s;
     if (capacity > 0) {
         const hipError_t e = fasgd::launch_scatter(cache, st->P, idx, val, d_count, capacity, stream);
         if (e != hipSuccess) return hip_fail(e, "bfasgd_apply_cached (cache update)");
@@ -618,8 +636,6 @@ fasgd_status bfasgd_apply_cached(fasgd_state* st, const int32_t* idx, const floa
     a.P = st->P;
     a.K = 1;
     a.h = hyper_of(st);
-    const bool vec = aligned(st->theta, 16) && aligned(st->n, 16) && aligned(st->b, 16) && aligned(st->v, 16) &&
-                     aligned(cache, 16);
     const hipError_t e = fasgd::launch_fasgd_dense(a, variant_of(st), vec, stream);
     if (e != hipSuccess) return hip_fail(e, "bfasgd_apply_cached");
     st->dense_T = st->T;

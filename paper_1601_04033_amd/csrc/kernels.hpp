@@ -34,6 +34,11 @@ hipError_t launch_sasgd_dense(const DenseArgs& a, bool aligned, hipStream_t s);
 // theta <- theta - coef[k] * (g_k / lambda), k in order (coef[k] = lr)
 hipError_t launch_sync_sgd(const DenseArgs& a, bool aligned, hipStream_t s);
 
+// Kernels with one parameter per thread (the paths for arrays that are only
+// 4-byte aligned) cover at most this many: a launch has fewer than 2^32
+// work-items.
+constexpr int64_t kMaxScalarItems = (int64_t(1) << 32) - 256;
+
 // B-FASGD selection: Philox decisions -> per-wave ballots and per-tile
 // counts, an exclusive scan of the tile counts, then ordered writes.
 struct SelectArgs {

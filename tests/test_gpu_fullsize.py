@@ -253,6 +253,49 @@ def test_dense_beyond_int32_parameters():
     _free()
 
 
+def test_dense_beyond_one_thread_per_parameter_limit():
+    """P = 2^32 + 5, past what a launch with one parameter per thread covers:
+    the state initialises (grid-stride), a one-gradient pass over aligned
+    arrays takes the vector kernel and matches the oracle on sampled indices
+    (with the ragged tail), and the same pass with one array off 16-byte
+    alignment is rejected on the host with nothing enqueued."""
+    import torch
+    dev = gpu()
+    P = 2 ** 32 + 5
+    free, _ = torch.cuda.mem_get_info()
+    if free < 130e9:
+        pytest.skip("needs about 130 GB of free device memory")
+    print(f"dense: P={P}", flush=True)
+    theta, n, b, v, last_T = fa.allocate_state(P, dev)
+    gen = torch.Generator(device=dev).manual_seed(7)
+    theta.normal_(0.0, 0.05, generator=gen)
+    st = fa.fasgd_init_state(theta, n, b, v, last_T, lam=4, alpha=0.005, math_mode=fa.MATH_FAST)
+    g = torch.empty(P, device=dev).normal_(0.0, 0.01, generator=gen)
+    js = np.unique(np.concatenate([np.arange(P - 70, P), sample_indices(P, 2048, seed=4)]))
+    jt = torch.from_numpy(js).to(dev)
+    ref = oracle.init_state(theta[jt].cpu().numpy(), alpha=0.005)
+    torch.cuda.synchronize()
+    assert (last_T[jt] == -1).all() and (v[jt] == 0).all() and (n[-8:] == 0).all()
+
+    # theta 4 bytes into a buffer one element longer: not 16-byte aligned,
+    # and in bounds even if a pass ran over it
+    tb = torch.empty(P + 1, device=dev)
+    c_bad = type(st.c).from_buffer_copy(st.c)
+    c_bad.theta = tb[1:].data_ptr()
+    bad = fa.State(c_bad, st.tensors)
+    with pytest.raises(fa.FasgdError) as err:
+        fa.fasgd_apply_updates(bad, [g], [0], [0])
+    assert err.value.status == 5 and bad.T == 0      # FASGD_ERR_ALIGN
+    del tb
+
+    fa.fasgd_apply_updates(st, [g], [1], [0])
+    oracle.fasgd_apply(ref, g[jt].cpu().numpy(), 0)
+    torch.cuda.synchronize()
+    assert_state_close(st, ref, RTOL_SEQ, js=jt, what="P > 2^32")
+    del g, st, theta, n, b, v, last_T
+    _free()
+
+
 @pytest.mark.parametrize("P", [64 * 1024 * 1024, 64 * 1024 * 1024 + 1])
 def test_select_at_group_scan_switch(P):
     """Selection is bit-exact on both sides of the switch between the fused
