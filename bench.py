@@ -558,8 +558,13 @@ def main():
     # widened paths at the same shape, after the timed region
     #   cached push: the list of the last push written into one client's cache,
     #   then the whole cache applied (Sec. 2.3's re-apply of dropped values)
+    #   (with the list's index: merged into the cache inside the one pass;
+    #   without it: the list copy, then the pass)
     extra = torch.zeros_like(pool[0])
-    cached_ms = timed(lambda: fa.bfasgd_apply_cached(st, idx, val, cnt, extra, clients[st.T], ts[st.T]))
+    fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, st.T, clients[st.T], idx, val, cnt, ws, seg_start=seg)
+    cached_ms = timed(lambda: fa.bfasgd_apply_cached(st, idx, val, cnt, extra, clients[st.T], ts[st.T],
+                                                     seg_start=seg))
+    cached_two_ms = timed(lambda: fa.bfasgd_apply_cached(st, idx, val, cnt, extra, clients[st.T], ts[st.T]))
     m_last = int(cnt.item())
     #   fetch: selection over the server's theta, copied into a client's copy
     def fetch():
@@ -642,7 +647,8 @@ def main():
             "sgd_sync_apply": {"ms": sync_ms, "lambda": K,
                                "GB/s": P * (8 + 4 * K) / (sync_ms * 1e-3) / 1e9},
             "bfasgd_apply_cached": {"ms": cached_ms, "transmitted": m_last,
-                                    "GB/s_algorithmic": (36 * P + 12 * m_last) / (cached_ms * 1e-3) / 1e9},
+                                    "GB/s_algorithmic": (36 * P + 12 * m_last) / (cached_ms * 1e-3) / 1e9,
+                                    "ms_two_steps": cached_two_ms},
             "fetch_select_and_copy": {"ms": fetch_ms, "transmitted": m_fetch,
                                       "GB/s_algorithmic": (8 * P + 20 * m_fetch) / (fetch_ms * 1e-3) / 1e9},
             "bfasgd_decide_segments": {"ms_whole_vector": dec1_ms, "ms_64_segments": dec64_ms,

@@ -87,7 +87,7 @@ def load_library(path: Optional[str] = None):
     lib.bfasgd_select_compact_batch.argtypes = [S, i32, P, f, f, u64, P, P, P, P, i64, P, P, P, sz, P]
     lib.fasgd_apply_pushes.argtypes = [S, i32, P, P, P, P, i64, P, P, P]
     lib.sgd_sync_apply.argtypes = [S, P, f, P]
-    lib.bfasgd_apply_cached.argtypes = [S, P, P, P, i64, P, i32, i64, P]
+    lib.bfasgd_apply_cached.argtypes = [S, P, P, P, P, i64, P, i32, i64, P]
     lib.bfasgd_apply_fetch.argtypes = [P, i64, P, P, P, i64, P]
     lib.bfasgd_segments_workspace_bytes.argtypes = [i64, i32]
     lib.bfasgd_segments_workspace_bytes.restype = sz
@@ -439,8 +439,11 @@ def sgd_sync_apply(state: State, grads: Sequence, lr: float, stream=None) -> Non
     _check(load_library().sgd_sync_apply(ctypes.byref(state.c), ptrs, lr, _stream(stream)))
 
 
-def bfasgd_apply_cached(state: State, idx, val, d_count, cache, client: int, grad_ts: int, stream=None) -> None:
-    """Push with dropped values re-applied from the client's cache (updated in place)."""
+def bfasgd_apply_cached(state: State, idx, val, d_count, cache, client: int, grad_ts: int, seg_start=None,
+                        stream=None) -> None:
+    """Push with dropped values re-applied from the client's cache (updated in
+    place).  seg_start (optional): the list's index from the selection, with
+    which the list is merged into the cache inside the one pass."""
     import torch
     cap = idx.numel()
     if val.numel() != cap:
@@ -449,8 +452,8 @@ def bfasgd_apply_cached(state: State, idx, val, d_count, cache, client: int, gra
         raise ValueError("cache length differs from P")
     rc = load_library().bfasgd_apply_cached(
         ctypes.byref(state.c), _dev_ptr(idx, torch.int32, "idx"), _dev_ptr(val, torch.float32, "val"),
-        _dev_ptr(d_count, torch.int64, "d_count"), cap, _dev_ptr(cache, torch.float32, "cache"),
-        int(client), int(grad_ts), _stream(stream))
+        _dev_ptr(d_count, torch.int64, "d_count"), _seg_start_ptr(seg_start, state.P), cap,
+        _dev_ptr(cache, torch.float32, "cache"), int(client), int(grad_ts), _stream(stream))
     _check(rc)
 
 

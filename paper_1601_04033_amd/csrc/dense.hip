@@ -273,6 +273,76 @@ __global__ __launch_bounds__(kBlock) void fasgd_dense_push_vec(const DenseArgs a
     }
 }
 
+// A push whose dropped values re-apply the client's most recent gradient
+// (Sec. 2.3) in one pass: every wave merges its segment's list entries into
+// the client's cache segment (staged as in the pass above), writes the
+// segment back whole when it has entries, and applies the merged values as
+// one gradient.  Bit for bit the list copy into the cache followed by a
+// one-gradient pass over it, without the partial-sector writes of the copy.
+template <int MODE>
+__global__ __launch_bounds__(kBlock) void fasgd_cached_push_vec(const DenseArgs a, const PushArgs p,
+                                                                float* __restrict__ cache)
+{
+    __shared__ float s_val[kWavesPerBlock][kPushSeg];
+    __shared__ uint32_t s_flag[kWavesPerBlock][kWave];    // byte c of word l: parameter 4 l + c listed
+    const Hyper h = a.h;
+    const int64_t nvec = a.P >> 2;
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int64_t seg = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + w;
+    const int64_t first = seg * kPushSeg;
+    const int64_t o = i * 4;
+    int64_t lo, hi;
+    push_range(p, seg, lo, hi);
+    int32_t e_idx = -1;
+    float e_val = 0.0f;
+    if (lo + lane < hi) { e_idx = p.idx[lo + lane]; e_val = p.val[lo + lane]; }
+    const bool own = i < nvec;
+    f4 th, n, b, v, cv;
+    if (own) {
+        th = ld4(a.theta + o); n = ld4(a.n + o); b = ld4(a.b + o); v = ld4(a.v + o);
+        cv = ld4(cache + o);
+    }
+    s_flag[w][lane] = 0u;
+    wave_lds_order();
+    {
+        const int64_t x = static_cast<int64_t>(e_idx) - first;
+        if (e_idx >= 0 && x >= 0 && x < kPushSeg && first + x < a.P) {
+            s_val[w][x] = e_val;
+            reinterpret_cast<uint8_t*>(s_flag[w])[x] = 1;
+        }
+    }
+    if (hi - lo > kWave)
+        stage_push(p, lo + kWave, hi, first, kPushSeg, a.P, s_val[w], reinterpret_cast<uint8_t*>(s_flag[w]), lane);
+    wave_lds_order();
+    const uint32_t flags = s_flag[w][lane];
+    const f4 pv = *reinterpret_cast<const f4*>(&s_val[w][4 * lane]);
+    if (own) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            if ((flags >> (8 * c)) & 0xffu) cv[c] = pv[c];
+        if (hi > lo) st4(cache + o, cv);       // the segment has entries (wave-uniform)
+        fasgd_step4<MODE>(th, n, b, v, cv, a.coef[0], h);
+        st4(a.theta + o, th);
+        st4(a.n + o, n);
+        st4(a.b + o, b);
+        st4(a.v + o, v);
+    } else if (i == nvec) {
+        for (int64_t j = nvec * 4; j < a.P; ++j) {
+            const int c = static_cast<int>(j - nvec * 4);
+            float gj = cache[j];
+            if ((flags >> (8 * c)) & 0xffu) {
+                gj = pv[c];
+                cache[j] = gj;
+            }
+            float tt = a.theta[j], nn = a.n[j], bb = a.b[j], vv = a.v[j];
+            fasgd_step<MODE>(tt, nn, bb, vv, gj, a.coef[0], h);
+            a.theta[j] = tt; a.n[j] = nn; a.b[j] = bb; a.v[j] = vv;
+        }
+    }
+}
+
 // The same, one parameter per thread (arrays only 4-byte aligned): a wave
 // covers 64 parameters, a quarter of a list-index segment.
 template <int MODE>
@@ -478,6 +548,19 @@ hipError_t launch_fasgd_dense(const DenseArgs& a, int variant, bool aligned, hip
     case kernel_variant(MATH_IEEE, 0): launch_dense_variant<kernel_variant(MATH_IEEE, 0)>(a, vec, grid, s); break;
     case kernel_variant(MATH_FAST, 1): launch_dense_variant<kernel_variant(MATH_FAST, 1)>(a, vec, grid, s); break;
     case kernel_variant(MATH_IEEE, 1): launch_dense_variant<kernel_variant(MATH_IEEE, 1)>(a, vec, grid, s); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_fasgd_cached_push(const DenseArgs& a, const PushArgs& p, float* cache, int variant, hipStream_t s)
+{
+    const unsigned grid = grid_for((a.P >> 2) + 1);
+    switch (variant) {
+    case kernel_variant(MATH_FAST, 0): fasgd_cached_push_vec<kernel_variant(MATH_FAST, 0)><<<grid, kBlock, 0, s>>>(a, p, cache); break;
+    case kernel_variant(MATH_IEEE, 0): fasgd_cached_push_vec<kernel_variant(MATH_IEEE, 0)><<<grid, kBlock, 0, s>>>(a, p, cache); break;
+    case kernel_variant(MATH_FAST, 1): fasgd_cached_push_vec<kernel_variant(MATH_FAST, 1)><<<grid, kBlock, 0, s>>>(a, p, cache); break;
+    case kernel_variant(MATH_IEEE, 1): fasgd_cached_push_vec<kernel_variant(MATH_IEEE, 1)><<<grid, kBlock, 0, s>>>(a, p, cache); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -604,16 +604,17 @@ fasgd_status sgd_sync_apply(fasgd_state* st, const float* const* grads, float lr
 }
 
 fasgd_status bfasgd_apply_cached(fasgd_state* st, const int32_t* idx, const float* val, const int64_t* d_count,
-                                 int64_t capacity, float* cache, int32_t client, int64_t grad_ts,
-                                 hipStream_t stream)
+                                 const uint32_t* seg_start, int64_t capacity, float* cache, int32_t client,
+                                 int64_t grad_ts, hipStream_t stream)
 {
     fasgd_status s = check_state(st, true);
     if (s != FASGD_OK) return s;
     if (!d_count || !cache) return fail(FASGD_ERR_NULL, "d_count or cache is NULL");
     if (capacity < 0) return fail(FASGD_ERR_ARG, "capacity must be >= 0");
     if (capacity > 0 && (!idx || !val)) return fail(FASGD_ERR_NULL, "idx or val is NULL");
-    if ((idx && !aligned(idx, 4)) || (val && !aligned(val, 4)) || !aligned(d_count, 8) || !aligned(cache, 4))
-        return fail(FASGD_ERR_ALIGN, "misaligned idx, val, d_count or cache");
+    if ((idx && !aligned(idx, 4)) || (val && !aligned(val, 4)) || !aligned(d_count, 8) || !aligned(cache, 4) ||
+        (seg_start && !aligned(seg_start, 4)))
+        return fail(FASGD_ERR_ALIGN, "misaligned idx, val, d_count, seg_start or cache");
     float tau_div;
     s = staleness(st, &client, &grad_ts, 1, &tau_div);
     if (s != FASGD_OK) return s;
@@ -621,6 +622,34 @@ fasgd_status bfasgd_apply_cached(fasgd_state* st, const int32_t* idx, const floa
                      aligned(cache, 16);
     s = scalar_size_ok(st->P, vec);
     if (s != FASGD_OK) return s;
+    const float coef = st->math_mode == FASGD_MATH_FAST ? st->alpha / tau_div : tau_div;
+    if (seg_start && vec) {
+        // one pass: the list merged into the cache segment by segment, then applied
+        fasgd::DenseArgs a;
+        memset(&a, 0, sizeof a);
+        a.theta = st->theta;
+        a.n = st->n;
+        a.b = st->b;
+        a.v = st->v;
+        a.grad[0] = cache;
+        a.coef[0] = coef;
+        a.P = st->P;
+        a.K = 1;
+        a.h = hyper_of(st);
+        fasgd::PushArgs p;
+        memset(&p, 0, sizeof p);
+        p.idx = idx;
+        p.val = val;
+        p.d_count = d_count;
+        p.seg_start = seg_start;
+        p.capacity = capacity;
+        p.n_segs = fasgd::push_segments(st->P);
+        const hipError_t e = fasgd::launch_fasgd_cached_push(a, p, cache, variant_of(st), stream);
+        if (e != hipSuccess) return hip_fail(e, "bfasgd_apply_cached");
+        st->dense_T = st->T;
+        st->T += 1;
+        return ok();
+    }
     if (capacity > 0) {
         const hipError_t e = fasgd::launch_scatter(cache, st->P, idx, val, d_count, capacity, stream);
         if (e != hipSuccess) return hip_fail(e, "bfasgd_apply_cached (cache update)");
@@ -632,7 +661,7 @@ fasgd_status bfasgd_apply_cached(fasgd_state* st, const int32_t* idx, const floa
     a.b = st->b;
     a.v = st->v;
     a.grad[0] = cache;
-    a.coef[0] = st->math_mode == FASGD_MATH_FAST ? st->alpha / tau_div : tau_div;
+    a.coef[0] = coef;
     a.P = st->P;
     a.K = 1;
     a.h = hyper_of(st);

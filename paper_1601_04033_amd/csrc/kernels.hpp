@@ -125,6 +125,10 @@ struct PushArgs {
 // decisions the pass then takes from the v it leaves (vector path only).
 hipError_t launch_fasgd_dense_push(const DenseArgs& a, const PushArgs& p, const SelectArgs* mark, int variant,
                                    bool aligned, hipStream_t s);
+// A cached push (dropped values re-apply the client's cache) in one pass over
+// 16-byte aligned arrays: the list (with its index) merged into the cache,
+// then the cache applied as one gradient (a.K = 1, a.coef[0]).
+hipError_t launch_fasgd_cached_push(const DenseArgs& a, const PushArgs& p, float* cache, int variant, hipStream_t s);
 
 // B compacted pushes applied in order in one pass (push b at timestamp
 // T0 + b); listed parameters get last_T = T0 + the last push that lists them.

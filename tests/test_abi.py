@@ -356,7 +356,7 @@ def test_next_entry_points_reject_bad_arguments(lib):
     cntp = (cnt.ctypes.data + 7) & ~7
 
     def cached(cache=f.ptr(5), client=0, ts=0, cap=16):
-        return lib.bfasgd_apply_cached(ctypes.byref(st), f.ptr(0), f.ptr(1), cntp, cap, cache, client, ts, None)
+        return lib.bfasgd_apply_cached(ctypes.byref(st), f.ptr(0), f.ptr(1), cntp, None, cap, cache, client, ts, None)
 
     assert cached(cache=None) == 1
     assert cached(ts=3) == 3

@@ -210,3 +210,62 @@ def test_mlp_per_tensor_pushes_sequence(mode):
     torch.cuda.synchronize()
     assert_state_close(st, ref, RTOL_SEQ, what="after 200 per-tensor pushes")
     assert 0 < sent < 200 * S
+
+
+@pytest.mark.parametrize("reading", [fa.V_EQUATIONS, fa.V_PROSE])
+@pytest.mark.parametrize("mode", [fa.MATH_FAST, fa.MATH_IEEE])
+@pytest.mark.parametrize("P,c_mult,cap_frac,offset", [(100_003, 2.0, 1.0, 0), (1_000_003, 8.0, 1.0, 0),
+                                                      (257, 0.0, 1.0, 0), (65_537, None, 1.0, 0),
+                                                      (200_003, 4.0, 0.05, 0), (65_537, 3.0, 1.0, 1)])
+def test_cached_push_in_one_pass_is_bit_identical(P, c_mult, cap_frac, offset, mode, reading):
+    """With the list's index the list is merged into the cache inside the
+    pass that applies it: the state, T, dense_T and the cache equal the list
+    copy followed by the one-gradient pass, bit for bit (a ragged tail,
+    everything sent, nothing sent, a capacity cut, and arrays 4 bytes off
+    16-byte alignment, which take the two steps)."""
+    import torch
+    dev = gpu()
+    rng = np.random.default_rng(P % 991)
+    theta0 = rng.normal(0.0, 0.05, P).astype(np.float32)
+    states, caches = [], []
+    for _ in range(2):
+        bufs = fa.allocate_state(P + offset, dev)
+        theta, n, b, v, last_T = (t[offset:] for t in bufs)
+        theta.copy_(torch.from_numpy(theta0))
+        st = fa.fasgd_init_state(theta, n, b, v, last_T, lam=8, alpha=0.005, math_mode=mode, v_reading=reading)
+        st.keep = bufs
+        states.append(st)
+        cb = torch.empty(P + offset, device=dev)
+        cb[offset:].copy_(torch.from_numpy((0.01 * rng.standard_normal(P)).astype(np.float32)) if not caches
+                          else caches[0])
+        caches.append(cb[offset:])
+    a, b = states
+    g0 = to_dev((0.01 * rng.standard_normal(P)).astype(np.float32), dev)
+    for st in (a, b):
+        fa.fasgd_apply_updates(st, [g0], [0], [0])
+    cap = max(1, int(P * cap_frac))
+    idx = torch.full((cap,), -1, device=dev, dtype=torch.int32)
+    val = torch.zeros(cap, device=dev)
+    cnt = torch.zeros(1, device=dev, dtype=torch.int64)
+    seg = torch.full((fa.bfasgd_list_index_length(P),), -1, device=dev, dtype=torch.int32)
+    g = to_dev((0.01 * rng.standard_normal(P)).astype(np.float32), dev)
+    # c as a multiple of the mean of v: about 1/(1 + c_mult) of the values are sent
+    c = 3e38 if c_mult is None else float(np.float32(c_mult * a.v.double().mean().item()))
+    fa.bfasgd_select_compact(a, g, c, 1e-8, SEED, a.T, 3, idx, val, cnt, fa.allocate_workspace(P, dev),
+                             seg_start=seg)
+    fa.bfasgd_apply_cached(a, idx, val, cnt, caches[0], 3, 0)
+    fa.bfasgd_apply_cached(b, idx, val, cnt, caches[1], 3, 0, seg_start=seg)
+    torch.cuda.synchronize()
+    m = int(cnt.item())
+    if c_mult == 0.0:
+        assert m == P
+    if c_mult is None:
+        assert m < P // 1000
+    if cap_frac < 1.0:
+        assert m > cap
+    if c_mult:
+        assert 0.5 / (1 + c_mult) < m / P < 2.0 / (1 + c_mult)
+    for name in ("theta", "n", "b", "v"):
+        assert torch.equal(a.tensors[name], b.tensors[name]), name
+    assert torch.equal(caches[0], caches[1])
+    assert a.T == b.T == 2 and a.dense_T == b.dense_T == 1
