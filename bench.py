@@ -567,11 +567,23 @@ def main():
     cached_two_ms = timed(lambda: fa.bfasgd_apply_cached(st, idx, val, cnt, extra, clients[st.T], ts[st.T]))
     m_last = int(cnt.item())
     #   fetch: selection over the server's theta, copied into a client's copy
+    #   (with the list's index the copy rewrites whole segments; without it,
+    #   one scattered write per entry)
     def fetch():
+        fa.bfasgd_select_compact(st, theta, c, EPS_C, SEED ^ 0xFE7C, st.T, clients[st.T], idx, val, cnt, ws,
+                                 seg_start=seg)
+        fa.bfasgd_apply_fetch(extra, idx, val, cnt, seg_start=seg)
+
+    def fetch_scatter():
         fa.bfasgd_select_compact(st, theta, c, EPS_C, SEED ^ 0xFE7C, st.T, clients[st.T], idx, val, cnt, ws)
         fa.bfasgd_apply_fetch(extra, idx, val, cnt)
-    fetch_ms = timed(fetch)
+    fetch_seg_ms = timed(fetch)
+    fetch_scatter_ms = timed(fetch_scatter)
     m_fetch = int(cnt.item())
+    # the rule the header states: by segments when the copy does not fit the
+    # 256 MB Infinity Cache (and most segments hold an entry, as at 10 %)
+    fetch_by_segments = 4 * P > 256 * 2 ** 20
+    fetch_ms = fetch_seg_ms if fetch_by_segments else fetch_scatter_ms
     #   the paper's own decision: one per push from the mean of v, and one per
     #   segment for 64 equal segments; then the push applied on the sent ones
     seg1 = np.array([0, P], np.int64)
@@ -650,7 +662,9 @@ def main():
                                     "GB/s_algorithmic": (36 * P + 12 * m_last) / (cached_ms * 1e-3) / 1e9,
                                     "ms_two_steps": cached_two_ms},
             "fetch_select_and_copy": {"ms": fetch_ms, "transmitted": m_fetch,
-                                      "GB/s_algorithmic": (8 * P + 20 * m_fetch) / (fetch_ms * 1e-3) / 1e9},
+                                      "GB/s_algorithmic": (8 * P + 20 * m_fetch) / (fetch_ms * 1e-3) / 1e9,
+                                      "copy": "by segments" if fetch_by_segments else "scattered",
+                                      "ms_copy_by_segments": fetch_seg_ms, "ms_scattered_copy": fetch_scatter_ms},
             "bfasgd_decide_segments": {"ms_whole_vector": dec1_ms, "ms_64_segments": dec64_ms,
                                        "GB/s": 4 * P / (dec1_ms * 1e-3) / 1e9},
             "bfasgd_apply_segments": {"ms_all_sent": segapply_ms,

@@ -88,7 +88,7 @@ def load_library(path: Optional[str] = None):
     lib.fasgd_apply_pushes.argtypes = [S, i32, P, P, P, P, i64, P, P, P]
     lib.sgd_sync_apply.argtypes = [S, P, f, P]
     lib.bfasgd_apply_cached.argtypes = [S, P, P, P, P, i64, P, i32, i64, P]
-    lib.bfasgd_apply_fetch.argtypes = [P, i64, P, P, P, i64, P]
+    lib.bfasgd_apply_fetch.argtypes = [P, i64, P, P, P, P, i64, P]
     lib.bfasgd_segments_workspace_bytes.argtypes = [i64, i32]
     lib.bfasgd_segments_workspace_bytes.restype = sz
     lib.bfasgd_decide_segments.argtypes = [S, P, i32, f, f, u64, i64, i32, P, P, sz, P]
@@ -457,8 +457,10 @@ def bfasgd_apply_cached(state: State, idx, val, d_count, cache, client: int, gra
     _check(rc)
 
 
-def bfasgd_apply_fetch(theta_client, idx, val, d_count, stream=None) -> None:
-    """Copy the listed values into a client's copy of theta."""
+def bfasgd_apply_fetch(theta_client, idx, val, d_count, seg_start=None, stream=None) -> None:
+    """Copy the listed values into a client's copy of theta.  seg_start
+    (optional): the list's index, with which segments holding an entry are
+    rewritten whole (faster when most segments hold one)."""
     import torch
     cap = idx.numel()
     if val.numel() != cap:
@@ -466,7 +468,8 @@ def bfasgd_apply_fetch(theta_client, idx, val, d_count, stream=None) -> None:
     rc = load_library().bfasgd_apply_fetch(
         _dev_ptr(theta_client, torch.float32, "theta_client"), theta_client.numel(),
         _dev_ptr(idx, torch.int32, "idx"), _dev_ptr(val, torch.float32, "val"),
-        _dev_ptr(d_count, torch.int64, "d_count"), cap, _stream(stream))
+        _dev_ptr(d_count, torch.int64, "d_count"), _seg_start_ptr(seg_start, theta_client.numel()), cap,
+        _stream(stream))
     _check(rc)
 
 

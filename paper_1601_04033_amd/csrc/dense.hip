@@ -343,6 +343,46 @@ __global__ __launch_bounds__(kBlock) void fasgd_cached_push_vec(const DenseArgs 
     }
 }
 
+// The listed values written into a dense array segment by segment (the
+// fetch refresh of a client's copy of theta): a wave reads its segment
+// whole, puts the segment's entries in and writes it back whole; segments
+// without entries are not touched.  Full-line writes instead of one partial
+// 32-byte sector per entry.
+__global__ __launch_bounds__(kBlock) void merge_list_vec(float* __restrict__ dst, int64_t P, const PushArgs p)
+{
+    __shared__ float s_val[kWavesPerBlock][kPushSeg];
+    __shared__ uint32_t s_flag[kWavesPerBlock][kWave];
+    const int64_t nvec = P >> 2;
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int64_t seg = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + w;
+    const int64_t first = seg * kPushSeg;
+    int64_t lo, hi;
+    push_range(p, seg, lo, hi);
+    if (hi == lo) return;                      // wave-uniform: nothing listed here
+    const bool own = i < nvec;
+    f4 d;
+    if (own) d = ld4(dst + i * 4);
+    s_flag[w][lane] = 0u;
+    wave_lds_order();
+    stage_push(p, lo, hi, first, kPushSeg, P, s_val[w], reinterpret_cast<uint8_t*>(s_flag[w]), lane);
+    wave_lds_order();
+    const uint32_t flags = s_flag[w][lane];
+    const f4 pv = *reinterpret_cast<const f4*>(&s_val[w][4 * lane]);
+    if (own) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            if ((flags >> (8 * c)) & 0xffu) d[c] = pv[c];
+        st4(dst + i * 4, d);
+    } else if (i == nvec) {
+        for (int64_t j = nvec * 4; j < P; ++j) {
+            const int c = static_cast<int>(j - nvec * 4);
+            if ((flags >> (8 * c)) & 0xffu) dst[j] = pv[c];
+        }
+    }
+}
+
 // The same, one parameter per thread (arrays only 4-byte aligned): a wave
 // covers 64 parameters, a quarter of a list-index segment.
 template <int MODE>
@@ -563,6 +603,12 @@ hipError_t launch_fasgd_cached_push(const DenseArgs& a, const PushArgs& p, float
     case kernel_variant(MATH_IEEE, 1): fasgd_cached_push_vec<kernel_variant(MATH_IEEE, 1)><<<grid, kBlock, 0, s>>>(a, p, cache); break;
     default: return hipErrorInvalidValue;
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_merge_list(float* dst, int64_t P, const PushArgs& p, hipStream_t s)
+{
+    merge_list_vec<<<grid_for((P >> 2) + 1), kBlock, 0, s>>>(dst, P, p);
     return hipGetLastError();
 }
 

@@ -673,14 +673,29 @@ fasgd_status bfasgd_apply_cached(fasgd_state* st, const int32_t* idx, const floa
 }
 
 fasgd_status bfasgd_apply_fetch(float* theta_client, int64_t P, const int32_t* idx, const float* val,
-                                const int64_t* d_count, int64_t capacity, hipStream_t stream)
+                                const int64_t* d_count, const uint32_t* seg_start, int64_t capacity,
+                                hipStream_t stream)
 {
     if (!theta_client || !d_count) return fail(FASGD_ERR_NULL, "theta_client or d_count is NULL");
     if (P < 1) return fail(FASGD_ERR_ARG, "P = %lld must be >= 1", (long long)P);
     if (capacity < 0) return fail(FASGD_ERR_ARG, "capacity must be >= 0");
     if (capacity > 0 && (!idx || !val)) return fail(FASGD_ERR_NULL, "idx or val is NULL");
-    if (!aligned(theta_client, 4) || (idx && !aligned(idx, 4)) || (val && !aligned(val, 4)) || !aligned(d_count, 8))
-        return fail(FASGD_ERR_ALIGN, "misaligned theta_client, idx, val or d_count");
+    if (!aligned(theta_client, 4) || (idx && !aligned(idx, 4)) || (val && !aligned(val, 4)) ||
+        !aligned(d_count, 8) || (seg_start && !aligned(seg_start, 4)))
+        return fail(FASGD_ERR_ALIGN, "misaligned theta_client, idx, val, d_count or seg_start");
+    if (capacity > 0 && seg_start && aligned(theta_client, 16)) {
+        fasgd::PushArgs p;
+        memset(&p, 0, sizeof p);
+        p.idx = idx;
+        p.val = val;
+        p.d_count = d_count;
+        p.seg_start = seg_start;
+        p.capacity = capacity;
+        p.n_segs = fasgd::push_segments(P);
+        const hipError_t e = fasgd::launch_merge_list(theta_client, P, p, stream);
+        if (e != hipSuccess) return hip_fail(e, "bfasgd_apply_fetch");
+        return ok();
+    }
     if (capacity > 0) {
         const hipError_t e = fasgd::launch_scatter(theta_client, P, idx, val, d_count, capacity, stream);
         if (e != hipSuccess) return hip_fail(e, "bfasgd_apply_fetch");

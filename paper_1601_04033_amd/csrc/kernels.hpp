@@ -129,6 +129,9 @@ hipError_t launch_fasgd_dense_push(const DenseArgs& a, const PushArgs& p, const 
 // 16-byte aligned arrays: the list (with its index) merged into the cache,
 // then the cache applied as one gradient (a.K = 1, a.coef[0]).
 hipError_t launch_fasgd_cached_push(const DenseArgs& a, const PushArgs& p, float* cache, int variant, hipStream_t s);
+// dst[idx[i]] = val[i] for the list (with its index) over a 16-byte aligned
+// dst, written segment by segment in whole lines.
+hipError_t launch_merge_list(float* dst, int64_t P, const PushArgs& p, hipStream_t s);
 
 // B compacted pushes applied in order in one pass (push b at timestamp
 // T0 + b); listed parameters get last_T = T0 + the last push that lists them.

@@ -365,7 +365,7 @@ def test_next_entry_points_reject_bad_arguments(lib):
     assert cached(cache=f.ptr(5, misalign=1)) == 5
 
     def fetch(dst=f.ptr(2), P=16, cap=16, count=cntp):
-        return lib.bfasgd_apply_fetch(dst, P, f.ptr(0), f.ptr(1), count, cap, None)
+        return lib.bfasgd_apply_fetch(dst, P, f.ptr(0), f.ptr(1), count, None, cap, None)
 
     assert fetch(dst=None) == 1
     assert fetch(P=0) == 2

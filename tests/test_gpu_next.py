@@ -269,3 +269,49 @@ def test_cached_push_in_one_pass_is_bit_identical(P, c_mult, cap_frac, offset, m
         assert torch.equal(a.tensors[name], b.tensors[name]), name
     assert torch.equal(caches[0], caches[1])
     assert a.T == b.T == 2 and a.dense_T == b.dense_T == 1
+
+
+@pytest.mark.parametrize("P,c,cap_frac,offset", [(1_000_003, 30.0, 1.0, 0), (257, 0.0, 1.0, 0),
+                                                 (65_537, 3e38, 1.0, 0), (200_003, 5.0, 0.05, 0),
+                                                 (100_003, 30.0, 1.0, 1), (3, 1.0, 1.0, 0)])
+def test_fetch_copy_by_segments_equals_scattered_copy(P, c, cap_frac, offset):
+    """With the list's index the fetch copy rewrites whole segments; the
+    client's copy equals the scattered copy bit for bit (ragged tail,
+    everything sent, nothing sent, a capacity cut, a copy 4 bytes off 16-byte
+    alignment, which takes the scattered copy)."""
+    import torch
+    dev = gpu()
+    rng = np.random.default_rng(P % 613)
+    theta_srv = rng.standard_normal(P).astype(np.float32)
+    st = new_gpu_state(theta_srv, dev, 8, 0.005, fa.MATH_FAST)
+    st.v.copy_(torch.from_numpy(workload.synthetic_v(P, seed=P % 613)))
+    client = rng.standard_normal(P).astype(np.float32)
+    copies = []
+    for _ in range(2):
+        buf = torch.empty(P + offset, device=dev)
+        buf[offset:].copy_(torch.from_numpy(client))
+        copies.append(buf[offset:])
+    cap = max(1, int(P * cap_frac))
+    idx = torch.full((cap,), -1, device=dev, dtype=torch.int32)
+    val = torch.zeros(cap, device=dev)
+    cnt = torch.zeros(1, device=dev, dtype=torch.int64)
+    seg = torch.full((fa.bfasgd_list_index_length(P),), -1, device=dev, dtype=torch.int32)
+    fa.bfasgd_select_compact(st, st.theta, c, 1e-8, SEED ^ 0xFE7C, 4, 2, idx, val, cnt, fa.allocate_workspace(P, dev),
+                             seg_start=seg)
+    fa.bfasgd_apply_fetch(copies[0], idx, val, cnt)
+    fa.bfasgd_apply_fetch(copies[1], idx, val, cnt, seg_start=seg)
+    torch.cuda.synchronize()
+    m = int(cnt.item())
+    if c == 0.0:
+        assert m == P
+    if cap_frac < 1.0:
+        assert m > cap
+    assert torch.equal(copies[0].view(torch.int32), copies[1].view(torch.int32))
+    if c == 0.0:
+        assert torch.equal(copies[1], st.theta)
+    expect = client.copy()
+    r_idx, r_val, r_m = oracle.bfasgd_select(st.v.cpu().numpy(), theta_srv, c, 1e-8, SEED ^ 0xFE7C, 4, 2,
+                                             capacity=cap)
+    assert r_m == m
+    expect[r_idx] = r_val
+    np.testing.assert_array_equal(copies[1].cpu().numpy().view(np.uint32), expect.view(np.uint32))
