@@ -355,23 +355,25 @@ def test_next_entry_points_reject_bad_arguments(lib):
     cnt = np.zeros(2, np.int64)
     cntp = (cnt.ctypes.data + 7) & ~7
 
-    def cached(cache=f.ptr(5), client=0, ts=0, cap=16):
-        return lib.bfasgd_apply_cached(ctypes.byref(st), f.ptr(0), f.ptr(1), cntp, None, cap, cache, client, ts, None)
+    def cached(cache=f.ptr(5), client=0, ts=0, cap=16, seg=None):
+        return lib.bfasgd_apply_cached(ctypes.byref(st), f.ptr(0), f.ptr(1), cntp, seg, cap, cache, client, ts, None)
 
     assert cached(cache=None) == 1
     assert cached(ts=3) == 3
     assert cached(client=3) == 4
     assert cached(cap=-1) == 2
     assert cached(cache=f.ptr(5, misalign=1)) == 5
+    assert cached(seg=f.ptr(4, misalign=2)) == 5          # the list index must be 4-byte aligned
 
-    def fetch(dst=f.ptr(2), P=16, cap=16, count=cntp):
-        return lib.bfasgd_apply_fetch(dst, P, f.ptr(0), f.ptr(1), count, None, cap, None)
+    def fetch(dst=f.ptr(2), P=16, cap=16, count=cntp, seg=None):
+        return lib.bfasgd_apply_fetch(dst, P, f.ptr(0), f.ptr(1), count, seg, cap, None)
 
     assert fetch(dst=None) == 1
     assert fetch(P=0) == 2
     assert fetch(cap=-3) == 2
     assert fetch(count=None) == 1
     assert fetch(dst=f.ptr(2, misalign=2)) == 5
+    assert fetch(seg=f.ptr(4, misalign=1)) == 5
     assert st.T == 2
 
 
