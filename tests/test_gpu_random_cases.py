@@ -20,7 +20,7 @@ import workload
 from helpers import RTOL_ONE, RTOL_SEQ, assert_close, assert_state_close, gpu, new_gpu_state, to_dev
 
 pytestmark = pytest.mark.gpu
-N_CASES = 48
+N_CASES = 64
 EDGES = (4, 256, 1024, 4096, 16384, 65536, 262144)
 
 
