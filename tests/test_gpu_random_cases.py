@@ -10,7 +10,9 @@ staleness), each held to the same bar as the enumerated tests:
  * a batch of pushes, selected and applied together, bit-identical to the
    single calls;
  * the widened paths: a synchronous SGD step, per-segment decisions and the
-   segment apply, a cached push and a fetch refresh, against the oracle."""
+   segment apply, a cached push and a fetch refresh, against the oracle;
+ * the cached push in one pass and the fetch copy by segments (with the
+   list's index) bit-identical to their plain forms."""
 import numpy as np
 import pytest
 
@@ -343,3 +345,46 @@ def test_random_widened_paths_match_oracle(case):
     assert int(c_d.item()) == fm
     copy_h[fi] = fv
     np.testing.assert_array_equal(copy_d.cpu().numpy().view(np.uint32), copy_h.view(np.uint32))
+
+
+@pytest.mark.parametrize("case", range(N_CASES))
+def test_random_indexed_copies_equal_plain_ones(case):
+    """Given the list's index, the cached push runs in one pass and the fetch
+    copy goes segment by segment: states, caches and copies equal those of
+    the plain forms bit for bit."""
+    import torch
+    rng = np.random.default_rng(6000 + case)
+    dev = gpu()
+    P = _size(rng, 2_000_000)
+    mode = int(rng.choice([fa.MATH_FAST, fa.MATH_IEEE]))
+    reading = int(rng.choice([fa.V_EQUATIONS, fa.V_PROSE]))
+    off = int(rng.random() < 0.2)
+    c_mult = float(rng.choice([0.0, 0.5, 2.0, 9.0, 50.0]))
+    seed = int(rng.integers(0, 2 ** 63))
+    print(f"case {case}: P={P} mode={mode} reading={reading} offset={off} c_mult={c_mult}", flush=True)
+    (a, keep_a), (b, keep_b) = _two_states(P, dev, rng, mode, reading, off)
+    cache_h = (0.01 * rng.standard_normal(P)).astype(np.float32)
+    caches = [_offset_view(cache_h, dev, off) for _ in range(2)]
+    c = float(np.float32(c_mult * a.v.double().mean().item()))
+    cap = P if rng.random() < 0.75 else int(rng.integers(1, P // 8 + 2))
+    L = fa.bfasgd_list_index_length(P)
+    idx = torch.full((cap,), -1, device=dev, dtype=torch.int32)
+    val = torch.zeros(cap, device=dev)
+    cnt = torch.zeros(1, device=dev, dtype=torch.int64)
+    seg = torch.full((L,), -1, device=dev, dtype=torch.int32)
+    g = to_dev(rng.standard_normal(P).astype(np.float32), dev)
+    client = int(rng.integers(0, 32))
+    fa.bfasgd_select_compact(a, g, c, 1e-8, seed, a.T, client, idx, val, cnt, fa.allocate_workspace(P, dev),
+                             seg_start=seg)
+    fa.bfasgd_apply_cached(a, idx, val, cnt, caches[0], client, 8)
+    fa.bfasgd_apply_cached(b, idx, val, cnt, caches[1], client, 8, seg_start=seg)
+    copy_h = rng.standard_normal(P).astype(np.float32)
+    copies = [_offset_view(copy_h, dev, off) for _ in range(2)]
+    fa.bfasgd_apply_fetch(copies[0], idx, val, cnt)
+    fa.bfasgd_apply_fetch(copies[1], idx, val, cnt, seg_start=seg)
+    torch.cuda.synchronize()
+    for name in ("theta", "n", "b", "v"):
+        assert torch.equal(a.tensors[name].view(torch.int32), b.tensors[name].view(torch.int32)), name
+    assert a.T == b.T == 10 and a.dense_T == b.dense_T == 9
+    assert torch.equal(caches[0].view(torch.int32), caches[1].view(torch.int32))
+    assert torch.equal(copies[0].view(torch.int32), copies[1].view(torch.int32))
