@@ -138,18 +138,22 @@ def test_mlp_fasgd_k16_sampled(mode):
 @pytest.mark.parametrize("K", [1, 8, 32])
 def test_large_25m_sampled(K):
     """P = 25,000,000 in 50 blocks of 500k, lambda = 64, uniform 0..2 lambda
-    delays; 64 updates in passes of K (FAST mode, the benchmarked one)."""
+    delays; the workload's whole sequence of 512 updates in passes of K (FAST
+    mode, the benchmarked one), checked within the whole-sequence tolerance
+    on 4096 sampled parameters after every 64 updates and at the end."""
     import torch
     dev = gpu()
     w = workload.WORKLOADS["large"]
+    assert w.updates == 512 and w.updates % K == 0
+    print(f"large 25M: K={K}, {w.updates} updates", flush=True)
     theta0, m, s = workload.device_params(w, dev)
-    clients, ts = workload.schedule(w, 64)
+    clients, ts = workload.schedule(w, w.updates)
     js = sample_indices(w.P, 4096)
     jt = torch.from_numpy(js).to(dev)
     st = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, fa.MATH_FAST)
     ref = oracle.init_state(theta0[jt].cpu().numpy(), alpha=w.alpha_fasgd)
     bufs = [torch.empty(w.P, device=dev) for _ in range(K)]
-    for p in range(64 // K):
+    for p in range(w.updates // K):
         for k in range(K):
             workload.device_gradient(w, m, s, p * K + k, out=bufs[k])
         sl = slice(p * K, (p + 1) * K)
@@ -159,8 +163,12 @@ def test_large_25m_sampled(K):
         if p == 0:
             torch.cuda.synchronize()
             assert_state_close(st, ref, RTOL_ONE if K == 1 else RTOL_SEQ, js=jt, what="first pass")
+        elif ((p + 1) * K) % 64 == 0:
+            torch.cuda.synchronize()
+            assert_state_close(st, ref, RTOL_SEQ, js=jt, what=f"after {(p + 1) * K} updates")
     torch.cuda.synchronize()
-    assert_state_close(st, ref, RTOL_SEQ, js=jt, what="after 64 updates")
+    assert st.T == w.updates
+    assert_state_close(st, ref, RTOL_SEQ, js=jt, what=f"after all {w.updates} updates")
     del bufs
     torch.cuda.empty_cache()
 

@@ -21,6 +21,49 @@ def _free():
     torch.cuda.empty_cache()
 
 
+def _oracle_whole_list(v, g, c, seed, T, client, chunk=1 << 26):
+    """The oracle's push list over the whole host vector, selected slice by
+    slice: the slice [j0, j0 + chunk) with index_base = j0 decides exactly
+    as the whole vector does there (the property
+    test_slices_with_index_base_reproduce_the_whole_selection pins), so the
+    slices' lists, shifted by j0 and joined, are the whole list.  The slices
+    run on several host threads (the oracle's calls release the GIL)."""
+    import os
+    from concurrent.futures import ThreadPoolExecutor
+    assert chunk % 4 == 0
+    P = v.shape[0]
+
+    def one(j0):
+        i, x, m = oracle.bfasgd_select(v[j0:j0 + chunk], g[j0:j0 + chunk], c, 1e-8, SEED, T, client,
+                                       index_base=j0)
+        assert m == i.shape[0]
+        return i.astype(np.int64) + j0, x, m
+
+    with ThreadPoolExecutor(max(1, min(16, os.cpu_count() or 1))) as ex:
+        parts = list(ex.map(one, range(0, P, chunk)))
+    return (np.concatenate([q[0] for q in parts]), np.concatenate([q[1] for q in parts]),
+            sum(q[2] for q in parts))
+
+
+def _assert_whole_list(idx, val, seg, m, v_host, g_host, c, T, client, what):
+    """Count, every index, every value bit and the whole list index of a GPU
+    push list against the oracle's selection from the same fp32 v."""
+    import time
+    t0 = time.time()
+    r_idx, r_val, r_m = _oracle_whole_list(v_host, g_host, c, SEED, T, client)
+    assert m == r_m, (what, m, r_m)
+    got_idx = idx[:m].cpu().numpy()
+    assert np.array_equal(got_idx.astype(np.int64), r_idx), what
+    got_val = val[:m].cpu().numpy()
+    assert np.array_equal(got_val.view(np.uint32), r_val.view(np.uint32)), what
+    P = v_host.shape[0]
+    want_seg = np.searchsorted(r_idx, np.arange(0, P + 255, 256, dtype=np.int64)[:(P + 255) // 256])
+    got_seg = seg.cpu().numpy().view(np.uint32).astype(np.int64)
+    assert np.array_equal(got_seg[:-1], want_seg), what
+    assert got_seg[-1] == m
+    print(f"{what}: whole list of {m} entries equals the oracle's ({time.time() - t0:.1f} s)", flush=True)
+
+
 def _calibrate_c(v, target):
     vd = np.asarray(v, np.float64) + 1e-8
     lo, hi = 0.0, 1e7
@@ -131,6 +174,10 @@ def test_memscale_1e9_fused_step_sampled():
     torch.cuda.synchronize()
     mm = int(cnt.item())
     assert 0.08 < mm / P < 0.12, mm / P
+    # the whole list against the oracle's selection from the same fp32 v
+    gK_host = grads[K].cpu().numpy()
+    _assert_whole_list(idx, val, seg, mm, st.v.cpu().numpy(), gK_host, c, st.T, int(clients[K]),
+                       "push selected after the first pass")
     # the index against the list, at sampled segments
     segs = np.unique(js // 256)
     starts = seg[torch.from_numpy(segs).to(dev)].long()
@@ -176,7 +223,10 @@ def test_memscale_1e9_fused_step_sampled():
     np.testing.assert_array_equal(got2, want2)
     vals = val[pos.clamp(max=m2 - 1)].cpu().numpy()
     np.testing.assert_array_equal(vals[want2].view(np.uint32), g_host[K][want2].view(np.uint32))
-    del grads, st, idx, val, ws, seg, lst
+    # the whole list the pass decided, against the oracle's selection from the v the pass left
+    _assert_whole_list(idx, val, seg, m2, st.v.cpu().numpy(), gK_host, c, st.T, int(clients[nxt]),
+                       "push decided inside the pass")
+    del grads, st, idx, val, ws, seg, lst, gK_host
     _free()
 
 
