@@ -89,20 +89,69 @@ def calibrate_c(v, target, n=1 << 20):
     return float(np.float32(c))
 
 
-def cpu_baseline(pool, theta0_host, clients, ts, c, w, K, P_s):
-    """The oracle (single-threaded C, fp64) on the first P_s parameters of the
-    same step: K dense updates, one selection, one sparse apply."""
+def host_cpu():
+    """The host's CPU model (from /proc/cpuinfo), its logical CPU count and
+    the CPUs this process may run on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, os.cpu_count(), sorted(os.sched_getaffinity(0))
+
+
+def _oracle_step(theta0, grads, clients, ts, c, w, K, index_base=0):
+    """One step of the oracle on a slice: K dense updates, the selection of
+    one push (decided from the slice's global indices), its sparse apply."""
     import numpy as np
     import oracle
-    grads = [g[:P_s].cpu().numpy() for g in pool]
-    st = oracle.init_state(theta0_host[:P_s], alpha=w.alpha_fasgd)
-    t0 = time.perf_counter()
+    st = oracle.init_state(theta0, alpha=w.alpha_fasgd)
     for k in range(K):
         oracle.fasgd_apply(st, grads[k], ts[k])
-    idx, val, m = oracle.bfasgd_select(st.v.astype(np.float32), grads[K], c, EPS_C, SEED, st.T, clients[K])
+    idx, val, m = oracle.bfasgd_select(st.v.astype(np.float32), grads[K], c, EPS_C, SEED, st.T, clients[K],
+                                       index_base=index_base)
     oracle.bfasgd_apply_sparse(st, idx, val, ts[K])
-    dt = time.perf_counter() - t0
-    return (P_s * K + m) / dt, dt, m
+    return m
+
+
+def cpu_baseline(pool, theta0_host, clients, ts, c, w, K, P_s):
+    """The oracle (single-threaded C, fp64) on the first P_s parameters of the
+    same step (K dense updates, one selection, one sparse apply), with the
+    calling thread pinned to one CPU; then the same function on all the CPUs
+    this process may use, each thread on its own slice of the index range (the
+    updates are elementwise and the decisions keyed by the global index, so
+    the slices together do exactly the work of the whole)."""
+    from concurrent.futures import ThreadPoolExecutor
+    model, n_cpu, allowed = host_cpu()
+    grads = [g[:P_s].cpu().numpy() for g in pool]
+    theta0 = theta0_host[:P_s]
+    core = allowed[-1]
+    os.sched_setaffinity(0, {core})          # this thread only: the oracle runs on it
+    try:
+        t0 = time.perf_counter()
+        m = _oracle_step(theta0, grads, clients, ts, c, w, K)
+        dt = time.perf_counter() - t0
+    finally:
+        os.sched_setaffinity(0, set(allowed))
+    n_thr = len(allowed)
+    bounds = [(P_s * i // n_thr) & ~3 for i in range(n_thr)] + [P_s]
+
+    def part(i):
+        a, b = bounds[i], bounds[i + 1]
+        return _oracle_step(theta0[a:b], [g[a:b] for g in grads], clients, ts, c, w, K, index_base=a)
+
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(n_thr) as ex:
+        m_all = sum(ex.map(part, range(n_thr)))
+    dt_all = time.perf_counter() - t0
+    assert m_all == m, (m_all, m)
+    return {"value": (P_s * K + m) / dt, "seconds": dt, "transmitted": m, "pinned_core": core,
+            "host_logical_cpus": n_cpu, "cpus_available": n_thr, "cpu_model": model,
+            "all_cores": {"value": (P_s * K + m) / dt_all, "threads": n_thr, "seconds": dt_all}}
 
 
 def large_25m(fa, workload, dev, mode, K=32, reps=20):
@@ -676,10 +725,14 @@ def main():
     }
     if args.cpu_params:
         P_s = min(args.cpu_params, P)
-        rate, dt, m_s = cpu_baseline(pool, theta0_host, clients, ts, c, w, K, P_s)
-        out["cpu_baseline"] = {"value": rate, "unit": "param-updates/s", "cores": 1, "kind": "oracle",
+        cb = cpu_baseline(pool, theta0_host, clients, ts, c, w, K, P_s)
+        out["cpu_baseline"] = {"value": cb["value"], "unit": "param-updates/s", "cores": 1, "kind": "oracle",
                                "sample": f"first {P_s} parameters of the same workload, one step "
-                                         f"({K} dense updates + 1 push, {m_s} transmitted), {dt:.1f} s"}
+                                         f"({K} dense updates + 1 push, {cb['transmitted']} transmitted), "
+                                         f"{cb['seconds']:.1f} s on one pinned CPU",
+                               "pinned_core": cb["pinned_core"], "host_logical_cpus": cb["host_logical_cpus"],
+                               "cpus_available": cb["cpus_available"], "cpu_model": cb["cpu_model"],
+                               "all_cores": cb["all_cores"]}
     print(json.dumps(out), flush=True)
 
 
