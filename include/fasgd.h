@@ -200,6 +200,31 @@ fasgd_status bfasgd_select_compact(const fasgd_state* st, const float* grad, flo
                                    int64_t* d_count, uint32_t* out_seg_start,
                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * bfasgd_select_compact without a workspace argument, for callers that
+ * cannot allocate device memory: code under HIP graph capture, serving
+ * loops that must not call hipMalloc, harnesses that forbid it.  The
+ * selection's scratch (ballot words, tile counts and offsets, group totals)
+ * lives in a fixed device array built into the library, one per GPU, of
+ * FASGD_NOALLOC_SCRATCH_BYTES bytes, which stays allocated until the process
+ * ends.  Its device address is looked up once per device on the first call
+ * made with that device current.  The call allocates nothing (no hipMalloc,
+ * no library allocation) and needs no initialisation of the array: the
+ * kernels clear what must start at zero.
+ * Arguments, results and errors as bfasgd_select_compact (same lists,
+ * counts and list index, bit for bit), plus FASGD_ERR_CAPACITY when P
+ * exceeds FASGD_NOALLOC_MAX_P (nothing is enqueued).
+ * Every call on a GPU uses that GPU's one array: calls that overlap on one
+ * GPU (on different streams, or from different threads, without ordering)
+ * race and may produce wrong lists.  Issue them on one stream, or order them.
+ */
+#define FASGD_NOALLOC_MAX_P 67108864LL            /* 2^26 parameters */
+#define FASGD_NOALLOC_SCRATCH_BYTES 8945920ULL    /* bfasgd_workspace_bytes(FASGD_NOALLOC_MAX_P) */
+fasgd_status bfasgd_select_compact_noalloc(const fasgd_state* st, const float* grad, float c, float eps_c,
+                                           uint64_t seed, int64_t T, int32_t client,
+                                           int32_t* out_idx, float* out_val, int64_t capacity,
+                                           int64_t* d_count, uint32_t* out_seg_start, hipStream_t stream);
+
 /* Entries of the list index bfasgd_select_compact writes for P parameters:
  * ceil(P / 256) + 1 (0 for P < 1). */
 int64_t bfasgd_list_index_length(int64_t P);

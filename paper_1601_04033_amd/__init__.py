@@ -38,8 +38,11 @@ ABI_FUNCTIONS = ("fasgd_init_state", "fasgd_apply_updates", "sasgd_apply_updates
                  "bfasgd_segments_workspace_bytes", "bfasgd_decide_segments", "bfasgd_apply_segments",
                  "bfasgd_list_index_length", "fasgd_apply_with_push",
                  "bfasgd_select_compact_batch", "fasgd_apply_pushes", "fasgd_apply_with_push_and_select",
-                 "fasgd_record_next_pass",
+                 "fasgd_record_next_pass", "bfasgd_select_compact_noalloc",
                  "fasgd_status_string", "fasgd_last_error")
+
+# bfasgd_select_compact_noalloc: the largest P its built-in scratch holds
+FASGD_NOALLOC_MAX_P = 1 << 26
 
 
 class FasgdError(RuntimeError):
@@ -78,6 +81,7 @@ def load_library(path: Optional[str] = None):
     lib.bfasgd_workspace_bytes.argtypes = [i64]
     lib.bfasgd_workspace_bytes.restype = sz
     lib.bfasgd_select_compact.argtypes = [S, P, f, f, u64, i64, i32, P, P, i64, P, P, P, sz, P]
+    lib.bfasgd_select_compact_noalloc.argtypes = [S, P, f, f, u64, i64, i32, P, P, i64, P, P, P]
     lib.bfasgd_list_index_length.argtypes = [i64]
     lib.bfasgd_list_index_length.restype = i64
     lib.fasgd_apply_with_push.argtypes = [S, P, P, P, P, i64, i32, i64, P, P, P, i32, P]
@@ -96,7 +100,7 @@ def load_library(path: Optional[str] = None):
     for name in ("fasgd_init_state", "fasgd_apply_updates", "sasgd_apply_updates",
                  "bfasgd_select_compact", "bfasgd_apply_sparse", "sgd_sync_apply",
                  "bfasgd_apply_cached", "bfasgd_apply_fetch", "bfasgd_decide_segments",
-                 "bfasgd_apply_segments", "fasgd_apply_with_push"):
+                 "bfasgd_apply_segments", "fasgd_apply_with_push", "bfasgd_select_compact_noalloc"):
         getattr(lib, name).restype = ctypes.c_int
     lib.fasgd_record_next_pass.argtypes = [P, P]
     lib.fasgd_status_string.argtypes = [ctypes.c_int]
@@ -272,6 +276,25 @@ def bfasgd_select_compact(state: State, grad, c: float, eps_c: float, seed: int,
         _dev_ptr(out_idx, torch.int32, "out_idx"), _dev_ptr(out_val, torch.float32, "out_val"), cap,
         _dev_ptr(d_count, torch.int64, "d_count"), _seg_start_ptr(seg_start, state.P),
         _dev_ptr(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
+    _check(rc)
+
+
+def bfasgd_select_compact_noalloc(state: State, grad, c: float, eps_c: float, seed: int, T: int, client: int,
+                                  out_idx, out_val, d_count, seg_start=None, stream=None) -> None:
+    """bfasgd_select_compact with the library's built-in per-device scratch
+    instead of a workspace (P <= FASGD_NOALLOC_MAX_P): for callers that
+    cannot allocate.  Calls that overlap on one GPU race on that scratch."""
+    import torch
+    cap = out_idx.numel()
+    if out_val.numel() != cap:
+        raise ValueError("out_idx and out_val must have the same capacity")
+    if grad.numel() != state.P:
+        raise ValueError("grad length differs from P")
+    rc = load_library().bfasgd_select_compact_noalloc(
+        ctypes.byref(state.c), _dev_ptr(grad, torch.float32, "grad"), c, eps_c,
+        int(seed) & (2 ** 64 - 1), int(T), int(client),
+        _dev_ptr(out_idx, torch.int32, "out_idx"), _dev_ptr(out_val, torch.float32, "out_val"), cap,
+        _dev_ptr(d_count, torch.int64, "d_count"), _seg_start_ptr(seg_start, state.P), _stream(stream))
     _check(rc)
 
 

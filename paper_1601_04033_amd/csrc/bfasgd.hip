@@ -566,12 +566,10 @@ __global__ __launch_bounds__(kListBlock) void scatter_list(float* __restrict__ d
 
 }  // namespace
 
-size_t select_workspace_bytes(int64_t P)
-{
-    const int64_t nt = n_tiles(P);
-    return align256(size_t(nt) * kTileWords * sizeof(uint64_t)) + 2 * align256(size_t(nt) * sizeof(uint32_t)) +
-           2 * align256(size_t(kMaxGroups) * sizeof(uint32_t)) + align256(sizeof(uint32_t));
-}
+static_assert(kSelTileParams == kChunksPerTile * 4 && kSelTileWords == kTileWords && kSelMaxGroups == kMaxGroups,
+              "the workspace size in kernels.hpp follows this file's layout");
+
+size_t select_workspace_bytes(int64_t P) { return select_workspace_bytes_for(P); }
 
 void select_workspace_layout(void* ws, int64_t P, SelectArgs& a)
 {

@@ -5,6 +5,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "../../include/fasgd.h"
 #include "kernels.hpp"
 
@@ -378,6 +380,66 @@ fasgd_status bfasgd_select_compact_batch(const fasgd_state* st, int32_t B, const
 {
     return select_common(st, B, grads, c, eps_c, seed, T, clients, out_idx, out_val, capacity, d_count,
                          out_seg_start, workspace, workspace_bytes, stream, "bfasgd_select_compact_batch");
+}
+
+}  // extern "C"
+
+namespace {
+
+// Scratch of bfasgd_select_compact_noalloc: the selection workspace of the
+// largest call it accepts, one copy per device, held until the process ends.
+// In host code this name is a stand-in for the device array, not its
+// address: the calls pass the device address that hipGetSymbolAddress
+// returns for the current device.
+static_assert(fasgd::select_workspace_bytes_for(FASGD_NOALLOC_MAX_P) == FASGD_NOALLOC_SCRATCH_BYTES,
+              "the header states the scratch size");
+static __device__ __align__(256) unsigned char scratch[FASGD_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 256;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices];   // device address of `scratch` on each device, once looked up
+
+fasgd_status device_scratch(void** out)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "bfasgd_select_compact_noalloc: hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(FASGD_ERR_ARG, "bfasgd_select_compact_noalloc: device %d is beyond the %d this library tracks", dev,
+                    kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol,
+                            "bfasgd_select_compact_noalloc: hipGetSymbolAddress(scratch)");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return FASGD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+fasgd_status bfasgd_select_compact_noalloc(const fasgd_state* st, const float* grad, float c, float eps_c,
+                                           uint64_t seed, int64_t T, int32_t client, int32_t* out_idx,
+                                           float* out_val, int64_t capacity, int64_t* d_count,
+                                           uint32_t* out_seg_start, hipStream_t stream)
+{
+    if (!st) return fail(FASGD_ERR_NULL, "state is NULL");
+    if (st->P > FASGD_NOALLOC_MAX_P)
+        return fail(FASGD_ERR_CAPACITY,
+                    "bfasgd_select_compact_noalloc: P = %lld exceeds the %lld parameters its built-in scratch "
+                    "holds; use bfasgd_select_compact with a workspace",
+                    (long long)st->P, (long long)FASGD_NOALLOC_MAX_P);
+    void* ws = nullptr;
+    const fasgd_status s = device_scratch(&ws);
+    if (s != FASGD_OK) return s;
+    return select_common(st, 1, &grad, c, eps_c, seed, &T, &client, out_idx, out_val, capacity, d_count,
+                         out_seg_start, ws, FASGD_NOALLOC_SCRATCH_BYTES, stream, "bfasgd_select_compact_noalloc");
 }
 
 fasgd_status bfasgd_apply_sparse(fasgd_state* st, const int32_t* idx, const float* val, const int64_t* d_count,

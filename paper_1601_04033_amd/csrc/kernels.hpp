@@ -78,6 +78,20 @@ struct SelectBatch {
     size_t ws_stride;       // workspace bytes per push
 };
 
+// Workspace of one selection: 16 ballot words (8 bytes each) per wave tile
+// of kSelTileParams parameters, a count and an offset per tile, the totals
+// and offsets of at most kSelMaxGroups groups of tiles, and an arrival
+// counter, each part 256-byte aligned.
+constexpr int64_t kSelTileParams = 1024;
+constexpr int kSelTileWords = 16;
+constexpr int kSelMaxGroups = 4096;
+constexpr size_t sel_align256(size_t x) { return (x + 255) & ~size_t(255); }
+constexpr size_t select_workspace_bytes_for(int64_t P)
+{
+    const size_t nt = static_cast<size_t>((P + kSelTileParams - 1) / kSelTileParams);
+    return sel_align256(nt * kSelTileWords * sizeof(uint64_t)) + 2 * sel_align256(nt * sizeof(uint32_t)) +
+           2 * sel_align256(size_t(kSelMaxGroups) * sizeof(uint32_t)) + sel_align256(sizeof(uint32_t));
+}
 size_t select_workspace_bytes(int64_t P);
 // Carve the workspace into ballots / tile counts / tile offsets.
 void select_workspace_layout(void* ws, int64_t P, SelectArgs& a);

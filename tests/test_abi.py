@@ -202,6 +202,23 @@ def test_select_rejects_bad_arguments(lib):
     st.index_base = 0
 
 
+def test_noalloc_select_rejects_sizes_beyond_its_scratch(lib):
+    # checked before the device is touched: no GPU needed
+    st, f = _state(P=fa.FASGD_NOALLOC_MAX_P + 1)
+    cnt = np.zeros(2, np.int64)
+    cntp = (cnt.ctypes.data + 7) & ~7
+    rc = lib.bfasgd_select_compact_noalloc(ctypes.byref(st), f.ptr(5), 1.0, 1e-8, 7, 0, 0, f.ptr(0), f.ptr(1),
+                                           16, cntp, None, None)
+    assert rc == 6
+    assert b"exceeds" in lib.fasgd_last_error()
+    assert lib.bfasgd_select_compact_noalloc(None, f.ptr(5), 1.0, 1e-8, 7, 0, 0, f.ptr(0), f.ptr(1), 16, cntp,
+                                             None, None) == 1
+    # the header's figures are the library's
+    text = open(HEADER).read()
+    assert f"FASGD_NOALLOC_MAX_P {fa.FASGD_NOALLOC_MAX_P}LL" in text
+    assert f"FASGD_NOALLOC_SCRATCH_BYTES {fa.bfasgd_workspace_bytes(fa.FASGD_NOALLOC_MAX_P)}ULL" in text
+
+
 def test_fused_push_rejects_bad_arguments(lib):
     st, f = _state(P=16, T=2)
     cnt = np.zeros(2, np.int64)
