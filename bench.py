@@ -683,7 +683,7 @@ def main():
                                f"FASGD updates and taking the next push's transmit decisions, then that push's "
                                f"compaction; {args.math} math",
                    "P": P, "K": K, "lambda": w.lam, "math": args.math, "transmit_fraction": f, "c": c},
-        "roofline": {"bound": "hbm", "kernel": "fasgd_dense_push_vec", "achieved": achieved,
+        "roofline": {"bound": "hbm", "kernel": "fasgd_dense_push_lane", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic, "algorithmic_bytes": pass_bytes},
         "kernels": {

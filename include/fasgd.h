@@ -19,10 +19,11 @@
  *     On any error nothing is enqueued and the state (including T) is
  *     unchanged; fasgd_last_error() then describes the problem.
  *   - Device arrays are plain, densely packed 1-D arrays of P elements in
- *     parameter order (structure of arrays).  4-byte alignment is required;
- *     16-byte alignment of every array (as torch allocations have) selects
- *     the vectorised kernels.  Without it the kernels take one parameter
- *     per thread and P is limited to 2^32 - 256 (FASGD_ERR_ALIGN beyond).
+ *     parameter order (structure of arrays).  4-byte alignment is required.
+ *     The kernels take one parameter per thread up to P = 2^32 - 256;
+ *     beyond that every array must be 16-byte aligned (as torch
+ *     allocations are: the kernels then take 4 parameters per thread),
+ *     otherwise the call returns FASGD_ERR_ALIGN.
  *   - Calls that share a state must be issued on one stream (or otherwise
  *     ordered by the caller); concurrent calls on one state race.
  */

@@ -5,14 +5,17 @@
 // synchronous-SGD step.
 //
 // Every update is elementwise and HBM-bound, so the kernels are plain
-// streaming passes: each thread owns 4 consecutive parameters (one 16-byte
-// vector per state array; one parameter for a single-gradient pass), loads
-// their state once, applies the K queued gradients in arrival order with the
-// state in registers, and stores the state once.  Measured on MI355X:
-//   - the grid covers the arrays exactly (one 16-byte chunk per thread) in
-//     blocks of 128 threads; grid-stride loops over a few thousand blocks
-//     lose 10-25 % of HBM bandwidth on streaming passes, and 128-thread
-//     blocks beat 256 by up to 8 % on short (25M-parameter) passes;
+// streaming passes: each thread loads its parameters' state once, applies
+// the K queued gradients in arrival order with the state in registers, and
+// stores the state once.  Below kMaxScalarItems parameters every pass runs
+// one parameter per thread (any 4-byte alignment); beyond it, where one
+// thread per parameter no longer fits a launch, 16-byte aligned arrays run 4
+// parameters per thread.  Measured on MI355X:
+//   - one parameter per thread with a few gradient loads in flight (few
+//     VGPRs, 16 waves per SIMD) beats 4 per thread (16-byte loads, 4-6
+//     waves per SIMD) by 5-10 % on the K-fused passes, see kLaneBlock;
+//   - the grid covers the arrays exactly; grid-stride loops over a few
+//     thousand blocks lose 10-25 % of HBM bandwidth on streaming passes;
 //   - every load and store is non-temporal: nothing is re-read within a
 //     pass, and streaming hints help the mixed read/write traffic most at
 //     small K;
@@ -26,8 +29,24 @@ namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-constexpr int kBlock = 128;        // measured best for the streaming passes (2 waves)
-constexpr int kBatch = 8;          // gradients loaded together before use
+constexpr int kBlock = 128;        // the 4-per-thread passes (2 waves)
+constexpr int kBatch = 8;          // their gradients loaded together before use
+
+// One parameter per thread: the form of every pass below kMaxScalarItems.
+// Measured on MI355X at K = 32 against 4 parameters per thread (78-104
+// VGPRs, 4-6 waves per SIMD), same box: the FASGD pass 648 against 714 us at
+// 25M parameters (77 % against 70 % of 8 TB/s) and 26.9 against 28.9 ms at
+// 1e9; at K = 8, 80 % against 73 %.  The FASGD pass loads its gradients
+// kLaneBatch at a time (25 VGPRs, 16 waves per SIMD; batches of 2, 4, 6
+// measured 2-7 % slower) in blocks of kLaneBlock threads (128 and 512: 2-5 %
+// slower).  The pass with a push, SASGD and synchronous SGD take 4 at a time
+// (measured best for each; SASGD 0.52 against 0.56 ms at 25M).
+constexpr int kLaneBlock = 256;
+constexpr int kLaneBatch = 3;
+constexpr int kPushBatch = 4;      // the pass with a push: 647 against 694 us at 25M with 3, 28.1 against 29.3 ms at 1e9
+constexpr int kSgdBatch = 4;       // SASGD and synchronous SGD
+
+unsigned lane_grid(int64_t P) { return static_cast<unsigned>((P + kLaneBlock - 1) / kLaneBlock); }
 
 __device__ __forceinline__ f4 ld4(const float* p)
 {
@@ -37,6 +56,8 @@ __device__ __forceinline__ void st4(float* p, f4 x)
 {
     __builtin_nontemporal_store(x, reinterpret_cast<f4*>(p));
 }
+__device__ __forceinline__ float ldnt(const float* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ void stnt(float* p, float x) { __builtin_nontemporal_store(x, p); }
 
 template <int MODE>
 __device__ __forceinline__ void fasgd_step4(f4& th, f4& n, f4& b, f4& v, const f4 g, float coef,
@@ -156,6 +177,8 @@ __device__ __forceinline__ void stage_push(const PushArgs& p, int64_t lo, int64_
     }
 }
 
+// The pass with a push, 4 parameters per thread, for 16-byte aligned
+// arrays beyond kMaxScalarItems parameters (below it fasgd_dense_push_lane).
 // MARK: the pass also takes the transmit decisions of the next push (Sec.
 // 2.3) from the v it leaves, i.e. the selection's mark step on the v that a
 // selection after the pass would read: one Philox call per chunk of 4, and
@@ -383,57 +406,138 @@ __global__ __launch_bounds__(kBlock) void merge_list_vec(float* __restrict__ dst
     }
 }
 
-// The same, one parameter per thread (arrays only 4-byte aligned): a wave
-// covers 64 parameters, a quarter of a list-index segment.
-template <int MODE>
-__global__ __launch_bounds__(kBlock) void fasgd_dense_push_scalar(const DenseArgs a, const PushArgs p)
+// Block barrier that orders the block's LDS accesses only: outstanding
+// global loads are not waited for.
+__device__ __forceinline__ void block_barrier_lds()
 {
-    __shared__ float s_val[kWavesPerBlock][kWave];
-    __shared__ uint8_t s_flag[kWavesPerBlock][kWave];
-    const Hyper h = a.h;
-    const int lane = threadIdx.x & (kWave - 1);
-    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int64_t first = static_cast<int64_t>(blockIdx.x) * kBlock + w * kWave;   // the wave's first parameter
-    const int64_t j = first + lane;
-    int64_t lo, hi;
-    push_range(p, first / kPushSeg, lo, hi);
-    s_flag[w][lane] = 0;
-    wave_lds_order();
-    stage_push(p, lo, hi, first, kWave, a.P, s_val[w], s_flag[w], lane);
-    wave_lds_order();
-    if (j >= a.P) return;
-    float th = a.theta[j], n = a.n[j], b = a.b[j], v = a.v[j];
-    if (s_flag[w][lane]) fasgd_step<MODE>(th, n, b, v, s_val[w][lane], p.coef, h);
-    for (int k = 0; k < a.K; ++k) fasgd_step<MODE>(th, n, b, v, a.grad[k][j], a.coef[k], h);
-    a.theta[j] = th; a.n[j] = n; a.b[j] = b; a.v[j] = v;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// Same update, one parameter per thread: for arrays that are only 4-byte
-// aligned, and for passes with one gradient (K = 1), where it measured
-// 3-8 % faster than 4 parameters per thread at 1e9 parameters and 2.5 %
-// at 25M (at K = 32 the two are within 1 %).
+// The pass with a compacted push applied ahead of the K gradients, one
+// parameter per thread (any 4-byte alignment).  Block s owns list-index
+// segment s (kPushSeg parameters).  Thread t loads entry lo + t of the
+// segment's list range [lo, hi) (a segment holds at most kPushSeg entries:
+// the indices are distinct) and stages it in the block's LDS, a value and a
+// flag byte at its parameter.  Every global load is issued by every thread
+// (addresses kept inside the arrays), so waits are for the loads they need.
+// MARK: the pass also takes the next push's transmit decisions from the v it
+// leaves: each thread draws the Philox call of its parameter's chunk of 4
+// and keeps the word of its parameter; the wave's ballot (64 parameters, 16
+// chunks) gives bits 16 w .. 16 w + 15 of each of the segment's 4 ballot
+// words (word c: bit c of each of the segment's 64 chunks), which lanes
+// 0..3 store as 16-bit pieces, in the layout the selection's mark launch
+// writes.
+template <int MODE, bool MARK>
+__global__ __launch_bounds__(kLaneBlock) void fasgd_dense_push_lane(const DenseArgs a, const PushArgs p,
+                                                                    const SelectArgs m)
+{
+    static_assert(kLaneBlock == kPushSeg, "a block covers one list-index segment");
+    __shared__ float s_val[kPushSeg];
+    __shared__ uint8_t s_flag[kPushSeg];
+    const Hyper h = a.h;
+    const int K = a.K;
+    const int t = threadIdx.x;
+    const int64_t seg = blockIdx.x;
+    const int64_t first = seg * kPushSeg;
+    const int64_t j = first + t;
+    const bool own = j < a.P;
+    const int64_t jl = own ? j : a.P - 1;      // loads stay inside [0, P)
+    int64_t lo, hi;
+    push_range(p, seg, lo, hi);
+    const bool entry = lo + t < hi;
+    const int64_t e = entry ? lo + t : 0;      // entry 0 is readable (the launcher sees to it)
+    const int32_t e_idx = p.idx[e];
+    const float e_val = p.val[e];
+    float th = ldnt(a.theta + jl), n = ldnt(a.n + jl), b = ldnt(a.b + jl), v = ldnt(a.v + jl);
+    const int k0 = K < kPushBatch ? K : kPushBatch;
+    float g0[kPushBatch];
+#pragma unroll
+    for (int u = 0; u < kPushBatch; ++u) g0[u] = ldnt(a.grad[u < k0 ? u : 0] + jl);
+    s_flag[t] = 0;
+    block_barrier_lds();
+    if (entry) {
+        const int64_t x = static_cast<int64_t>(e_idx) - first;
+        if (x >= 0 && x < kPushSeg && first + x < a.P) {
+            s_val[x] = e_val;
+            s_flag[x] = 1;
+        }
+    }
+    block_barrier_lds();
+    if (s_flag[t]) fasgd_step<MODE>(th, n, b, v, s_val[t], p.coef, h);
+#pragma unroll
+    for (int u = 0; u < kPushBatch; ++u)
+        if (u < k0) fasgd_step<MODE>(th, n, b, v, g0[u], a.coef[u], h);
+    int k = k0;
+    for (; k + kPushBatch <= K; k += kPushBatch) {
+        float g[kPushBatch];
+#pragma unroll
+        for (int u = 0; u < kPushBatch; ++u) g[u] = ldnt(a.grad[k + u] + jl);
+#pragma unroll
+        for (int u = 0; u < kPushBatch; ++u) fasgd_step<MODE>(th, n, b, v, g[u], a.coef[k + u], h);
+    }
+    for (; k < K; ++k) fasgd_step<MODE>(th, n, b, v, ldnt(a.grad[k] + jl), a.coef[k], h);
+    if (own) {
+        stnt(a.theta + j, th);
+        stnt(a.n + j, n);
+        stnt(a.b + j, b);
+        stnt(a.v + j, v);
+    }
+    if (MARK) {
+        if (blockIdx.x == 0 && t == 0) *m.groups_done = 0u;   // for the scan launch
+        const int lane = t & (kWave - 1);
+        const int w = __builtin_amdgcn_readfirstlane(t / kWave);
+        uint32_t bit = 0;
+        if (own) {
+            const uint64_t qg = m.chunk_base + static_cast<uint64_t>(j >> 2);   // global chunk index
+            const uint4 wd = philox4x32_10(
+                make_uint4(static_cast<uint32_t>(qg), static_cast<uint32_t>(qg >> 32), m.ctr_T, m.ctr_client),
+                m.key0, m.key1);
+            const int c = static_cast<int>(j & 3);
+            const uint32_t word = c == 0 ? wd.x : c == 1 ? wd.y : c == 2 ? wd.z : wd.w;
+            bit = transmit_bit(word, v, m.c, m.eps_c);
+        }
+        // bit l: parameter first + 64 w + l, bit (l mod 4) of the segment's chunk 16 w + l / 4
+        const uint64_t wave_bits = __builtin_amdgcn_ballot_w64(bit != 0);
+        uint32_t piece = 0;   // lane c < 4: bits 16 w .. 16 w + 15 of the segment's word c
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const uint64_t wc = __builtin_amdgcn_ballot_w64(lane < 16 && ((wave_bits >> (4 * lane + c)) & 1u) != 0);
+            if (lane == c) piece = static_cast<uint32_t>(wc) & 0xFFFFu;
+        }
+        const int64_t tile_segs = m.n_tiles * 4;   // segments the ballot array holds
+        if (seg < tile_segs && lane < 4)
+            reinterpret_cast<uint16_t*>(m.ballots + seg * 4 + lane)[w] = static_cast<uint16_t>(piece);
+        // segments of the last tile beyond the grid hold no parameter: no bits
+        if (seg == static_cast<int64_t>(gridDim.x) - 1 && w == 0 && lane < 4)
+            for (int64_t s2 = seg + 1; s2 < tile_segs; ++s2) m.ballots[s2 * 4 + lane] = 0;
+    }
+}
+
+// K-fused FASGD, one parameter per thread (any 4-byte alignment): the pass
+// for every P below kMaxScalarItems.
 template <int MODE>
-__global__ __launch_bounds__(kBlock) void fasgd_dense_scalar(const DenseArgs a)
+__global__ __launch_bounds__(kLaneBlock) void fasgd_dense_lane(const DenseArgs a)
 {
     const Hyper h = a.h;
     const int K = a.K;
-    const int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    const int64_t j = static_cast<int64_t>(blockIdx.x) * kLaneBlock + threadIdx.x;
     if (j >= a.P) return;
-    float th = __builtin_nontemporal_load(a.theta + j), n = __builtin_nontemporal_load(a.n + j);
-    float b = __builtin_nontemporal_load(a.b + j), v = __builtin_nontemporal_load(a.v + j);
+    float th = ldnt(a.theta + j), n = ldnt(a.n + j), b = ldnt(a.b + j), v = ldnt(a.v + j);
     int k = 0;
-    for (; k + kBatch <= K; k += kBatch) {
-        float g[kBatch];
+    for (; k + kLaneBatch <= K; k += kLaneBatch) {
+        float g[kLaneBatch];
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) g[u] = __builtin_nontemporal_load(a.grad[k + u] + j);
+        for (int u = 0; u < kLaneBatch; ++u) g[u] = ldnt(a.grad[k + u] + j);
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) fasgd_step<MODE>(th, n, b, v, g[u], a.coef[k + u], h);
+        for (int u = 0; u < kLaneBatch; ++u) fasgd_step<MODE>(th, n, b, v, g[u], a.coef[k + u], h);
     }
-    for (; k < K; ++k) fasgd_step<MODE>(th, n, b, v, __builtin_nontemporal_load(a.grad[k] + j), a.coef[k], h);
-    __builtin_nontemporal_store(th, a.theta + j);
-    __builtin_nontemporal_store(n, a.n + j);
-    __builtin_nontemporal_store(b, a.b + j);
-    __builtin_nontemporal_store(v, a.v + j);
+    for (; k < K; ++k) fasgd_step<MODE>(th, n, b, v, ldnt(a.grad[k] + j), a.coef[k], h);
+    stnt(a.theta + j, th);
+    stnt(a.n + j, n);
+    stnt(a.b + j, b);
+    stnt(a.v + j, v);
 }
 
 // K-fused SASGD: theta <- theta - (alpha / tau_k) g_k; coef[k] = alpha / tau_k.
@@ -473,13 +577,30 @@ __global__ __launch_bounds__(kBlock) void sasgd_dense_vec(const DenseArgs a)
     }
 }
 
-__global__ __launch_bounds__(kBlock) void sasgd_dense_scalar(const DenseArgs a)
+// SYNC: synchronous SGD (the apply-update listing of Sec. 3), every gradient
+// divided by lambda before the step; otherwise K-fused SASGD.  One parameter
+// per thread, below kMaxScalarItems.
+template <bool SYNC>
+__global__ __launch_bounds__(kLaneBlock) void sgd_dense_lane(const DenseArgs a)
 {
-    const int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    const int K = a.K;
+    const float lam = a.lambda;
+    const int64_t j = static_cast<int64_t>(blockIdx.x) * kLaneBlock + threadIdx.x;
     if (j >= a.P) return;
-    float th = a.theta[j];
-    for (int k = 0; k < a.K; ++k) th = fmaf(-a.coef[k], a.grad[k][j], th);
-    a.theta[j] = th;
+    float th = ldnt(a.theta + j);
+    int k = 0;
+    for (; k + kSgdBatch <= K; k += kSgdBatch) {
+        float g[kSgdBatch];
+#pragma unroll
+        for (int u = 0; u < kSgdBatch; ++u) g[u] = ldnt(a.grad[k + u] + j);
+#pragma unroll
+        for (int u = 0; u < kSgdBatch; ++u) th = fmaf(-a.coef[k + u], SYNC ? g[u] / lam : g[u], th);
+    }
+    for (; k < K; ++k) {
+        const float g = ldnt(a.grad[k] + j);
+        th = fmaf(-a.coef[k], SYNC ? g / lam : g, th);
+    }
+    stnt(a.theta + j, th);
 }
 
 // Synchronous SGD (the apply-update listing of Sec. 3): every gradient is
@@ -521,14 +642,6 @@ __global__ __launch_bounds__(kBlock) void sync_sgd_vec(const DenseArgs a)
     }
 }
 
-__global__ __launch_bounds__(kBlock) void sync_sgd_scalar(const DenseArgs a)
-{
-    const int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-    if (j >= a.P) return;
-    float th = a.theta[j];
-    for (int k = 0; k < a.K; ++k) th = fmaf(-a.coef[k], a.grad[k][j] / a.lambda, th);
-    a.theta[j] = th;
-}
 
 }  // namespace
 
@@ -539,37 +652,49 @@ hipError_t launch_init(float* n, float* b, float* v, int32_t* last_T, int64_t P,
     return hipGetLastError();
 }
 
+// one parameter per thread below kMaxScalarItems; beyond it (16-byte
+// aligned arrays only: the API rejects others first) 4 per thread
 template <int VARIANT>
-void launch_dense_variant(const DenseArgs& a, bool aligned, unsigned grid, hipStream_t s)
+void launch_dense_variant(const DenseArgs& a, hipStream_t s)
 {
-    if (aligned)
-        fasgd_dense_vec<VARIANT><<<grid, kBlock, 0, s>>>(a);
+    if (a.P <= kMaxScalarItems)
+        fasgd_dense_lane<VARIANT><<<lane_grid(a.P), kLaneBlock, 0, s>>>(a);
     else
-        fasgd_dense_scalar<VARIANT><<<grid, kBlock, 0, s>>>(a);
+        fasgd_dense_vec<VARIANT><<<grid_for((a.P >> 2) + 1), kBlock, 0, s>>>(a);
 }
 
 template <int VARIANT>
-void launch_push_variant(const DenseArgs& a, const PushArgs& p, const SelectArgs* m, bool aligned, unsigned grid,
-                         hipStream_t s)
+void launch_push_variant(const DenseArgs& a, const PushArgs& p, const SelectArgs* m, hipStream_t s)
 {
-    if (m)
-        fasgd_dense_push_vec<VARIANT, true><<<grid, kBlock, 0, s>>>(a, p, *m);
-    else if (aligned)
-        fasgd_dense_push_vec<VARIANT, false><<<grid, kBlock, 0, s>>>(a, p, SelectArgs{});
-    else
-        fasgd_dense_push_scalar<VARIANT><<<grid, kBlock, 0, s>>>(a, p);
+    if (a.P <= kMaxScalarItems) {
+        // every thread reads list entry 0 or later: a list without capacity
+        // (its pointers may be NULL) reads the list index instead, which has
+        // at least two entries; no entry is then used
+        PushArgs q = p;
+        if (q.capacity == 0 || !q.idx || !q.val) {
+            q.idx = reinterpret_cast<const int32_t*>(q.seg_start);
+            q.val = reinterpret_cast<const float*>(q.seg_start);
+        }
+        if (m)
+            fasgd_dense_push_lane<VARIANT, true><<<lane_grid(a.P), kLaneBlock, 0, s>>>(a, q, *m);
+        else
+            fasgd_dense_push_lane<VARIANT, false><<<lane_grid(a.P), kLaneBlock, 0, s>>>(a, q, SelectArgs{});
+    } else if (m) {
+        fasgd_dense_push_vec<VARIANT, true><<<grid_for((a.P >> 2) + 1), kBlock, 0, s>>>(a, p, *m);
+    } else {
+        fasgd_dense_push_vec<VARIANT, false><<<grid_for((a.P >> 2) + 1), kBlock, 0, s>>>(a, p, SelectArgs{});
+    }
 }
 
 hipError_t launch_fasgd_dense_push(const DenseArgs& a, const PushArgs& p, const SelectArgs* mark, int variant,
                                    bool aligned, hipStream_t s)
 {
-    if (mark && !aligned) return hipErrorInvalidValue;   // the decisions ride on the vector kernel only
-    const unsigned grid = aligned ? grid_for((a.P >> 2) + 1) : grid_for(a.P);
+    if (a.P > kMaxScalarItems && !aligned) return hipErrorInvalidValue;   // the API rejects this first
     switch (variant) {
-    case kernel_variant(MATH_FAST, 0): launch_push_variant<kernel_variant(MATH_FAST, 0)>(a, p, mark, aligned, grid, s); break;
-    case kernel_variant(MATH_IEEE, 0): launch_push_variant<kernel_variant(MATH_IEEE, 0)>(a, p, mark, aligned, grid, s); break;
-    case kernel_variant(MATH_FAST, 1): launch_push_variant<kernel_variant(MATH_FAST, 1)>(a, p, mark, aligned, grid, s); break;
-    case kernel_variant(MATH_IEEE, 1): launch_push_variant<kernel_variant(MATH_IEEE, 1)>(a, p, mark, aligned, grid, s); break;
+    case kernel_variant(MATH_FAST, 0): launch_push_variant<kernel_variant(MATH_FAST, 0)>(a, p, mark, s); break;
+    case kernel_variant(MATH_IEEE, 0): launch_push_variant<kernel_variant(MATH_IEEE, 0)>(a, p, mark, s); break;
+    case kernel_variant(MATH_FAST, 1): launch_push_variant<kernel_variant(MATH_FAST, 1)>(a, p, mark, s); break;
+    case kernel_variant(MATH_IEEE, 1): launch_push_variant<kernel_variant(MATH_IEEE, 1)>(a, p, mark, s); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -577,17 +702,12 @@ hipError_t launch_fasgd_dense_push(const DenseArgs& a, const PushArgs& p, const 
 
 hipError_t launch_fasgd_dense(const DenseArgs& a, int variant, bool aligned, hipStream_t s)
 {
-    // vector path (nvec chunks plus one thread for the tail) for K > 1 over
-    // 16-byte aligned arrays, and for any K beyond the one-per-thread limit;
-    // one parameter per thread otherwise
-    const bool vec = aligned && (a.K > 1 || a.P > kMaxScalarItems);
-    if (!vec && a.P > kMaxScalarItems) return hipErrorInvalidValue;   // the API rejects this first
-    const unsigned grid = vec ? grid_for((a.P >> 2) + 1) : grid_for(a.P);
+    if (a.P > kMaxScalarItems && !aligned) return hipErrorInvalidValue;   // the API rejects this first
     switch (variant) {
-    case kernel_variant(MATH_FAST, 0): launch_dense_variant<kernel_variant(MATH_FAST, 0)>(a, vec, grid, s); break;
-    case kernel_variant(MATH_IEEE, 0): launch_dense_variant<kernel_variant(MATH_IEEE, 0)>(a, vec, grid, s); break;
-    case kernel_variant(MATH_FAST, 1): launch_dense_variant<kernel_variant(MATH_FAST, 1)>(a, vec, grid, s); break;
-    case kernel_variant(MATH_IEEE, 1): launch_dense_variant<kernel_variant(MATH_IEEE, 1)>(a, vec, grid, s); break;
+    case kernel_variant(MATH_FAST, 0): launch_dense_variant<kernel_variant(MATH_FAST, 0)>(a, s); break;
+    case kernel_variant(MATH_IEEE, 0): launch_dense_variant<kernel_variant(MATH_IEEE, 0)>(a, s); break;
+    case kernel_variant(MATH_FAST, 1): launch_dense_variant<kernel_variant(MATH_FAST, 1)>(a, s); break;
+    case kernel_variant(MATH_IEEE, 1): launch_dense_variant<kernel_variant(MATH_IEEE, 1)>(a, s); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -614,19 +734,23 @@ hipError_t launch_merge_list(float* dst, int64_t P, const PushArgs& p, hipStream
 
 hipError_t launch_sasgd_dense(const DenseArgs& a, bool aligned, hipStream_t s)
 {
-    if (aligned)
+    if (a.P <= kMaxScalarItems)
+        sgd_dense_lane<false><<<lane_grid(a.P), kLaneBlock, 0, s>>>(a);
+    else if (aligned)
         sasgd_dense_vec<<<grid_for((a.P >> 2) + 1), kBlock, 0, s>>>(a);
     else
-        sasgd_dense_scalar<<<grid_for(a.P), kBlock, 0, s>>>(a);
+        return hipErrorInvalidValue;   // the API rejects this first
     return hipGetLastError();
 }
 
 hipError_t launch_sync_sgd(const DenseArgs& a, bool aligned, hipStream_t s)
 {
-    if (aligned)
+    if (a.P <= kMaxScalarItems)
+        sgd_dense_lane<true><<<lane_grid(a.P), kLaneBlock, 0, s>>>(a);
+    else if (aligned)
         sync_sgd_vec<<<grid_for((a.P >> 2) + 1), kBlock, 0, s>>>(a);
     else
-        sync_sgd_scalar<<<grid_for(a.P), kBlock, 0, s>>>(a);
+        return hipErrorInvalidValue;   // the API rejects this first
     return hipGetLastError();
 }
 

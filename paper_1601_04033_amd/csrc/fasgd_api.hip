@@ -563,18 +563,12 @@ fasgd_status fasgd_apply_with_push_and_select(fasgd_state* st, const int32_t* pu
     s = select_setup(&after, 1, &next_grad, c, eps_c, seed, &T_next, &next_client, out_idx, out_val, out_capacity,
                      out_count, out_seg_start, workspace, workspace_bytes, m, bt, sel_vec);
     if (s != FASGD_OK) return s;
+    // the pass takes the decisions; the selection's own launches scan them
+    // and scatter
     hipError_t e = pass_begin(stream);
-    if (vec) {
-        // the pass takes the decisions; the selection's own launches scan
-        // them and scatter
-        if (e == hipSuccess) e = fasgd::launch_fasgd_dense_push(a, p, &m, variant_of(st), true, stream);
-        if (e == hipSuccess) e = pass_end(stream);
-        if (e == hipSuccess) e = fasgd::launch_select_after_mark(m, aligned(next_grad, 16), stream);
-    } else {
-        if (e == hipSuccess) e = fasgd::launch_fasgd_dense_push(a, p, nullptr, variant_of(st), false, stream);
-        if (e == hipSuccess) e = pass_end(stream);
-        if (e == hipSuccess) e = fasgd::launch_select(m, bt, 1, sel_vec, stream);
-    }
+    if (e == hipSuccess) e = fasgd::launch_fasgd_dense_push(a, p, &m, variant_of(st), vec, stream);
+    if (e == hipSuccess) e = pass_end(stream);
+    if (e == hipSuccess) e = fasgd::launch_select_after_mark(m, aligned(next_grad, 16), stream);
     if (e != hipSuccess) return hip_fail(e, "fasgd_apply_with_push_and_select");
     st->dense_T = st->T + K;
     st->T += K + 1;

@@ -136,7 +136,8 @@ struct PushArgs {
 };
 
 // mark: optional; the selection arguments of the next push, whose transmit
-// decisions the pass then takes from the v it leaves (vector path only).
+// decisions the pass then takes from the v it leaves.  aligned: every array
+// 16-byte aligned (needed only beyond kMaxScalarItems parameters).
 hipError_t launch_fasgd_dense_push(const DenseArgs& a, const PushArgs& p, const SelectArgs* mark, int variant,
                                    bool aligned, hipStream_t s);
 // A cached push (dropped values re-apply the client's cache) in one pass over

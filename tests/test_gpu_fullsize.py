@@ -305,9 +305,10 @@ def test_dense_beyond_int32_parameters():
 
 def test_dense_beyond_one_thread_per_parameter_limit():
     """P = 2^32 + 5, past what a launch with one parameter per thread covers:
-    the state initialises (grid-stride), a one-gradient pass over aligned
-    arrays takes the vector kernel and matches the oracle on sampled indices
-    (with the ragged tail), and the same pass with one array off 16-byte
+    the state initialises (grid-stride), the passes over aligned arrays take
+    the 4-per-thread kernels (FASGD with one and two gradients, a push ahead
+    of a gradient, SASGD, synchronous SGD) and match the oracle on sampled
+    indices (with the ragged tail), and a pass with one array off 16-byte
     alignment is rejected on the host with nothing enqueued."""
     import torch
     dev = gpu()
@@ -338,10 +339,43 @@ def test_dense_beyond_one_thread_per_parameter_limit():
     assert err.value.status == 5 and bad.T == 0      # FASGD_ERR_ALIGN
     del tb
 
+    g_s = g[jt].cpu().numpy()
     fa.fasgd_apply_updates(st, [g], [1], [0])
-    oracle.fasgd_apply(ref, g[jt].cpu().numpy(), 0)
+    oracle.fasgd_apply(ref, g_s, 0)
     torch.cuda.synchronize()
     assert_state_close(st, ref, RTOL_SEQ, js=jt, what="P > 2^32")
+    fa.fasgd_apply_updates(st, [g, g], [2, 3], [1, 0])
+    for ts in (1, 0):
+        oracle.fasgd_apply(ref, g_s, ts)
+    torch.cuda.synchronize()
+    assert_state_close(st, ref, RTOL_SEQ, js=jt, what="P > 2^32, K = 2")
+    # a push (every third sampled index below 2^31: the list holds int32
+    # indices) ahead of one gradient, in one pass
+    pos = np.flatnonzero(js < 2 ** 31)[::3]
+    push_j = js[pos].astype(np.int32)
+    push_v = (np.random.default_rng(5).standard_normal(pos.size) * 0.02).astype(np.float32)
+    seg_start = np.searchsorted(push_j.astype(np.int64), np.arange(0, P + 255, 256, dtype=np.int64))
+    seg_start = np.append(seg_start[:fa.bfasgd_list_index_length(P) - 1], push_j.size).astype(np.int32)
+    d_idx, d_val = torch.from_numpy(push_j).to(dev), torch.from_numpy(push_v).to(dev)
+    d_cnt = torch.tensor([push_j.size], device=dev, dtype=torch.int64)
+    d_seg = torch.from_numpy(seg_start).to(dev)
+    T0 = st.T
+    fa.fasgd_apply_with_push(st, d_idx, d_val, d_cnt, d_seg, 1, T0 - 1, [g], [2], [T0])
+    oracle.bfasgd_apply_sparse(ref, pos.astype(np.int32), push_v, T0 - 1)
+    oracle.fasgd_apply(ref, g_s, T0)
+    torch.cuda.synchronize()
+    assert_state_close(st, ref, RTOL_SEQ, js=jt, what="P > 2^32, push then gradient")
+    del d_idx, d_val, d_cnt, d_seg, seg_start
+    T1 = st.T
+    fa.sasgd_apply_updates(st, [g, g], [0, 3], [T1 - 2, T1])
+    oracle.sasgd_apply(ref, g_s, T1 - 2)
+    oracle.sasgd_apply(ref, g_s, T1)
+    fa.sgd_sync_apply(st, [g] * 4, 0.01)
+    oracle.sync_sgd_apply(ref, [g_s] * 4, 0.01)
+    torch.cuda.synchronize()
+    # SASGD and synchronous SGD move theta only
+    assert_close(st.theta[jt].cpu().numpy(), ref.theta, RTOL_SEQ, what="P > 2^32, SASGD and sync SGD theta")
+    assert st.T == ref.T
     del g, st, theta, n, b, v, last_T
     _free()
 
