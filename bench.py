@@ -532,6 +532,19 @@ def main():
         sp_ms.append(e[2].elapsed_time(e[3]))
     sep_ms_avg = float(np.mean(sep_ms[1:]))
     sp_ms = float(np.mean(sp_ms[1:]))
+    # the same push applied segment by segment with its list index
+    # (fasgd_apply_pushes with one push)
+    seg_ms = []
+    for r in range(3):
+        base = st.T
+        fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, st.T, clients[base], idx, val, cnt, ws, seg_start=seg)
+        a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        fa.fasgd_apply_pushes(st, idx.view(1, -1), val.view(1, -1), cnt, seg.view(1, -1), [clients[base]], [ts[base]])
+        b_.record()
+        torch.cuda.synchronize()
+        seg_ms.append(a.elapsed_time(b_))
+    sp_seg_ms = float(np.mean(seg_ms[1:]))
     # and as two calls: the pass with the queued push, then the full
     # selection (which reads v again)
     two_ms = []
@@ -703,7 +716,8 @@ def main():
                                       "GB/s_back_to_back": sel_b2b_bytes / (sel_b2b_ms * 1e-3) / 1e9,
                                       "frac_back_to_back": sel_b2b_bytes / (sel_b2b_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
                                       "transmitted_fraction": m_avg / P},
-            "bfasgd_apply_sparse": {"ms": sp_ms, "GB/s_algorithmic": sp_bytes / (sp_ms * 1e-3) / 1e9},
+            "bfasgd_apply_sparse": {"ms": sp_ms, "GB/s_algorithmic": sp_bytes / (sp_ms * 1e-3) / 1e9,
+                                    "ms_by_segments": sp_seg_ms},
             "sasgd_apply_updates": {"ms": sas_ms_avg, "GB/s": sas_bytes / (sas_ms_avg * 1e-3) / 1e9},
             "sgd_sync_apply": {"ms": sync_ms, "lambda": K,
                                "GB/s": P * (8 + 4 * K) / (sync_ms * 1e-3) / 1e9},

@@ -263,7 +263,13 @@ fasgd_status bfasgd_select_compact_batch(const fasgd_state* st, int32_t B, const
  * follow bfasgd_select_compact on the same stream without a host
  * round-trip).  Unlisted parameters keep theta, n, b, v and last_T; listed
  * ones get last_T = T.  T advances by one even when the list is empty.
- * Indices must be distinct; an index outside [0, P) is skipped.
+ * Indices must be distinct; an index outside [0, P) is skipped.  Each
+ * entry is one gather and one scatter of the listed parameter's state.  A
+ * list that comes with its index (bfasgd_select_compact's out_seg_start)
+ * can instead be applied segment by segment by fasgd_apply_pushes with
+ * B = 1, with the same result: faster above a few percent transmitted
+ * (1e9 parameters, 10 %: 7.2 against 9.4 ms), slower below (1.8 %: 4.9
+ * against 3.6 ms).
  *   idx, val  device int32 / fp32 [capacity]
  *   d_count   device int64 [1]
  * Errors: as fasgd_apply_updates with K = 1.
@@ -335,7 +341,10 @@ fasgd_status fasgd_apply_with_push_and_select(fasgd_state* st, const int32_t* pu
  * B-1, push b at timestamp T + b with staleness T + b - grad_ts[b], but
  * each parameter's state is read and written once.  A parameter listed by
  * some push gets last_T = T + the last such b; T advances by B; dense_T is
- * unchanged.
+ * unchanged.  With B = 1 this is bfasgd_apply_sparse applied segment by
+ * segment through the list's index: a segment the push lists nothing of is
+ * skipped, one with 8 or more entries is read and rewritten whole, one
+ * with fewer touches its listed parameters only.
  *   idx, val       device int32 / fp32 [B][capacity]; list b as
  *                  bfasgd_select_compact writes it (ascending, distinct)
  *   d_count        device int64 [B]
