@@ -89,6 +89,14 @@ def calibrate_c(v, target, n=1 << 20):
     return float(np.float32(c))
 
 
+def fetch_copy_by_segments(P, m):
+    """The rule bfasgd_apply_fetch's header states for its optional list
+    index: copy by segments when the client's copy does not fit the 256 MB
+    Infinity Cache and the transmitted fraction is above a few percent (most
+    segments then hold an entry), otherwise scatter one value per entry."""
+    return 4 * P > 256 * 2 ** 20 and m >= 0.05 * P
+
+
 def host_cpu():
     """The host's CPU model (from /proc/cpuinfo), its logical CPU count and
     the CPUs this process may run on."""
@@ -642,9 +650,7 @@ def main():
     fetch_seg_ms = timed(fetch)
     fetch_scatter_ms = timed(fetch_scatter)
     m_fetch = int(cnt.item())
-    # the rule the header states: by segments when the copy does not fit the
-    # 256 MB Infinity Cache (and most segments hold an entry, as at 10 %)
-    fetch_by_segments = 4 * P > 256 * 2 ** 20
+    fetch_by_segments = fetch_copy_by_segments(P, m_fetch)
     fetch_ms = fetch_seg_ms if fetch_by_segments else fetch_scatter_ms
     #   the paper's own decision: one per push from the mean of v, and one per
     #   segment for 64 equal segments; then the push applied on the sent ones

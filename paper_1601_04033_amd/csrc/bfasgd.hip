@@ -512,8 +512,8 @@ constexpr int64_t kListMaxBlocks = 65536;     // grid cap of the list kernels (g
 
 // A wave owns 64 E consecutive list entries and lane l takes entries
 // l, l + 64, ...: every gather instruction covers 64 consecutive entries
-// (ascending indices, so few cache lines), and each thread issues all 4 E of
-// its gathers before the first update.
+// (ascending indices, so few cache lines), and each thread issues all
+// kSparseE of its gathers before the first update.
 template <int MODE>
 __global__ __launch_bounds__(kListBlock) void sparse_apply(const SparseArgs a)
 {

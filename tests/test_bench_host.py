@@ -47,3 +47,12 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode != 0
     assert "one GPU" in (r.stdout + r.stderr)
+
+
+def test_fetch_copy_rule_follows_the_header():
+    # by segments only when the copy does not fit the 256 MB Infinity Cache and
+    # most segments hold an entry (a transmitted fraction of a few percent)
+    P = 1_000_000_000
+    assert bench.fetch_copy_by_segments(P, P // 10)
+    assert not bench.fetch_copy_by_segments(P, P // 100)
+    assert not bench.fetch_copy_by_segments(25_000_000, 2_500_000)
