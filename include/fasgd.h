@@ -381,10 +381,11 @@ fasgd_status sgd_sync_apply(fasgd_state* st, const float* const* grads, float lr
  * gradient at timestamp T with staleness T - grad_ts.  dense_T = T, T += 1.
  * Indices outside [0, P) are skipped.
  *   seg_start  optional (NULL: not used) device uint32, the list's index as
- *              bfasgd_select_compact writes it.  With it, and with the state
- *              and the cache 16-byte aligned, the list is merged into the
- *              cache inside the one pass that applies it (the same state
- *              and cache bit for bit, without a separate scattered copy).
+ *              bfasgd_select_compact writes it.  With it (and, beyond
+ *              2^32 - 256 parameters, the state and the cache 16-byte
+ *              aligned), the list is merged into the cache inside the one
+ *              pass that applies it (the same state and cache bit for bit,
+ *              without a separate scattered copy).
  * Errors: as bfasgd_apply_sparse, and FASGD_ERR_NULL for a NULL cache.
  */
 fasgd_status bfasgd_apply_cached(fasgd_state* st, const int32_t* idx, const float* val,

@@ -679,7 +679,7 @@ fasgd_status bfasgd_apply_cached(fasgd_state* st, const int32_t* idx, const floa
     s = scalar_size_ok(st->P, vec);
     if (s != FASGD_OK) return s;
     const float coef = st->math_mode == FASGD_MATH_FAST ? st->alpha / tau_div : tau_div;
-    if (seg_start && vec) {
+    if (seg_start && (vec || st->P <= fasgd::kMaxScalarItems)) {
         // one pass: the list merged into the cache segment by segment, then applied
         fasgd::DenseArgs a;
         memset(&a, 0, sizeof a);

@@ -304,3 +304,51 @@ def test_mlp_bfasgd_batched_sequence_sampled():
                        what="after 2000 pushes in batches of 16")
     assert 0.15 < np.mean(fractions) < 0.35, np.mean(fractions)
 
+
+
+def _host_list(P, dev, seed):
+    """A list built on the host with its index: segment s (256 parameters)
+    lists COUNTS[s mod len] distinct parameters (fewer in the ragged last
+    segment), ascending, with random values."""
+    import torch
+    rng = np.random.default_rng(seed)
+    counts = [0, 1, 7, 8, 9, 63, 64, 65, 128, 255, 256, 2, 0, 16]
+    idx = []
+    for s in range(-(-P // 256)):
+        lo, hi = 256 * s, min(256 * s + 256, P)
+        k = min(counts[s % len(counts)], hi - lo)
+        idx.append(np.sort(rng.choice(np.arange(lo, hi), size=k, replace=False)))
+    idx = np.concatenate(idx).astype(np.int32)
+    val = (rng.standard_normal(idx.size) * 0.02).astype(np.float32)
+    seg = np.searchsorted(idx.astype(np.int64), np.arange(0, P + 255, 256, dtype=np.int64)[:-(-P // 256)])
+    seg = np.append(seg, idx.size).astype(np.int32)
+    return idx, val, torch.from_numpy(seg).to(dev)
+
+
+@pytest.mark.parametrize("reading", [fa.V_EQUATIONS, fa.V_PROSE])
+@pytest.mark.parametrize("mode", [fa.MATH_FAST, fa.MATH_IEEE])
+@pytest.mark.parametrize("offset", [0, 1])
+@pytest.mark.parametrize("cut", ["none", "mid_segment", "half"])
+def test_single_push_by_segments_equals_sparse_apply(cut, offset, mode, reading):
+    """fasgd_apply_pushes with one push applies it segment by segment (whole
+    segments from 8 entries on, listed parameters only below, empty ones
+    skipped): theta, n, b, v, last_T (earlier values kept where nothing is
+    listed) and T equal bfasgd_apply_sparse's bit for bit, at the threshold
+    (7, 8, 9 entries), for full segments, a ragged last segment, misaligned
+    arrays and lists cut by capacity."""
+    import torch
+    dev = gpu()
+    P = 256 * 41 + 77
+    (a, b), _, _, keep = _mid_run_state(P, dev, mode, reading, seed=5, offset=offset)
+    idx_h, val_h, seg = _host_list(P, dev, seed=6)
+    m = idx_h.size
+    cap = {"none": m, "mid_segment": int(seg[20].item()) + 3, "half": m // 2}[cut]
+    idx = torch.full((1, max(cap, 1)), -1, device=dev, dtype=torch.int32)
+    val = torch.zeros((1, max(cap, 1)), device=dev)
+    idx[0, :cap] = torch.from_numpy(idx_h[:cap]).to(dev)
+    val[0, :cap] = torch.from_numpy(val_h[:cap]).to(dev)
+    cnt = torch.tensor([m], device=dev, dtype=torch.int64)       # the count may exceed the capacity
+    fa.bfasgd_apply_sparse(a, idx[0], val[0], cnt, 3, 38)
+    fa.fasgd_apply_pushes(b, idx, val, cnt, seg.view(1, -1), [3], [38])
+    _assert_same(a, b)
+    assert b.T == 41
