@@ -12,8 +12,8 @@
 // thread per parameter no longer fits a launch, 16-byte aligned arrays run 4
 // parameters per thread.  Measured on MI355X:
 //   - one parameter per thread with a few gradient loads in flight (few
-//     VGPRs, 16 waves per SIMD) beats 4 per thread (16-byte loads, 4-6
-//     waves per SIMD) by 5-10 % on the K-fused passes, see kLaneBlock;
+//     VGPRs, the full 8 waves per SIMD) beats 4 per thread (16-byte loads,
+//     4-6 waves per SIMD) by 5-10 % on the K-fused passes, see kLaneBlock;
 //   - the grid covers the arrays exactly; grid-stride loops over a few
 //     thousand blocks lose 10-25 % of HBM bandwidth on streaming passes;
 //   - every load and store is non-temporal: nothing is re-read within a
@@ -37,10 +37,11 @@ constexpr int kBatch = 8;          // their gradients loaded together before use
 // VGPRs, 4-6 waves per SIMD), same box: the FASGD pass 648 against 714 us at
 // 25M parameters (77 % against 70 % of 8 TB/s) and 26.9 against 28.9 ms at
 // 1e9; at K = 8, 80 % against 73 %.  The FASGD pass loads its gradients
-// kLaneBatch at a time (25 VGPRs, 16 waves per SIMD; batches of 2, 4, 6
-// measured 2-7 % slower) in blocks of kLaneBlock threads (128 and 512: 2-5 %
-// slower).  The pass with a push, SASGD and synchronous SGD take 4 at a time
-// (measured best for each; SASGD 0.52 against 0.56 ms at 25M).
+// kLaneBatch at a time (25 VGPRs, 8 waves per SIMD, the most a SIMD holds;
+// batches of 2, 4, 6 measured 2-7 % slower) in blocks of kLaneBlock threads
+// (128 and 512: 2-5 % slower).  The pass with a push, SASGD and synchronous
+// SGD take 4 at a time (measured best for each; SASGD 0.52 against 0.56 ms
+// at 25M).
 constexpr int kLaneBlock = 256;
 constexpr int kLaneBatch = 3;
 constexpr int kPushBatch = 4;      // the pass with a push: 647 against 694 us at 25M with 3, 28.1 against 29.3 ms at 1e9
