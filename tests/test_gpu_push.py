@@ -174,11 +174,12 @@ def _selection_buffers(P, cap, dev):
 def test_push_pass_and_next_selection_are_bit_identical(P, K, offset, cap_frac, base, mode):
     """fasgd_apply_with_push_and_select against fasgd_apply_with_push, then
     bfasgd_select_compact at the timestamp after the pass: the state, T,
-    dense_T, the next push's count, list and list index bit for bit.  Covers
-    ragged tails, P a multiple of 1024 (the thread after the last chunk
-    starts a segment past the ballot array), a shard offset, a capacity cut,
-    arrays 4 bytes off alignment (pass and selection as separate launches)
-    and more than 64 scan groups."""
+    dense_T, the next push's count, list and list index bit for bit.  The
+    pass takes the next push's decisions itself at every size and alignment.
+    Covers ragged tails (a last segment shorter than 256, a last tile whose
+    later segments hold no parameter), P a multiple of 1024, a shard offset,
+    a capacity cut, arrays 4 bytes off alignment and more than 64 scan
+    groups."""
     import torch
     dev = gpu()
     a, b, _, (m_, s_, w), keep = _states(P, dev, mode, fa.V_EQUATIONS, seed=P % 991, offset=offset)
