@@ -336,20 +336,30 @@ __device__ __forceinline__ void load_tile_grad(const SelectArgs& a, int64_t tile
     }
 }
 
-// The tile's entries, with gradients g, to list positions from `base` on.
-// Chunks past P carry no ballot bits, so their (unloaded) gradients are never
-// read.
+// The tile's ballot words (wave-uniform, scalar loads).  Loaded together
+// with the gradients, ahead of any use: loading them segment by segment
+// left up to three dependent scalar round trips in each wave's lifetime.
+__device__ __forceinline__ void load_tile_ballots(const SelectArgs& a, int64_t tile, uint64_t (&bw)[kTileWords])
+{
+    const uint64_t* tb = a.ballots + tile * kTileWords;
+#pragma unroll
+    for (int k = 0; k < kTileWords; ++k) bw[k] = tb[k];
+}
+
+// The tile's entries, with gradients g and ballot words bw (loaded into
+// registers already, or the tile's words in the workspace), to list
+// positions from `base` on.  Chunks past P carry no ballot bits, so their
+// (unloaded) gradients are never read.
 __device__ __forceinline__ void scatter_loaded(const SelectArgs& a, int64_t tile, int lane, const f4 (&g)[kTileSegs],
-                                               int64_t base, int32_t* s_idx, float* s_val)
+                                               const uint64_t* bw, int64_t base, int32_t* s_idx, float* s_val)
 {
     const int64_t q0 = tile * kChunksPerTile + lane;
-    const uint64_t* tb = a.ballots + tile * kTileWords;
     const uint64_t below = lanes_below(lane);
     uint32_t staged = 0;
     uint32_t seg_pos = 0;   // lane s < kTileSegs: list position of segment s's first entry
 #pragma unroll
     for (int s = 0; s < kTileSegs; ++s) {
-        const uint64_t b0 = tb[4 * s], b1 = tb[4 * s + 1], b2 = tb[4 * s + 2], b3 = tb[4 * s + 3];
+        const uint64_t b0 = bw[4 * s], b1 = bw[4 * s + 1], b2 = bw[4 * s + 2], b3 = bw[4 * s + 3];
         const uint32_t nib = static_cast<uint32_t>((b0 >> lane) & 1) | static_cast<uint32_t>(((b1 >> lane) & 1) << 1) |
                              static_cast<uint32_t>(((b2 >> lane) & 1) << 2) |
                              static_cast<uint32_t>(((b3 >> lane) & 1) << 3);
@@ -385,17 +395,41 @@ __device__ __forceinline__ void scatter_loaded(const SelectArgs& a, int64_t tile
     }
 }
 
-template <bool FULL>
+// EARLY: every ballot word and the list position are loaded and waited for
+// while the gradient loads are in flight.  In calls of at most
+// kFusedTopGroups groups (up to 67M parameters) every wave's latency is
+// exposed, and this took the 25M selection from 44.0-46.6 to 41.5-45.1 us
+// (same box, lists identical).  Otherwise the compiler issues each part
+// where it is first used (three dependent scalar round trips per tile),
+// which was 3 % faster at 1e9 (1.63-1.65 against 1.70 ms), where many more
+// waves are in flight to cover them.
+template <bool FULL, bool EARLY>
 __device__ __forceinline__ void scatter_tile(const SelectArgs& a, int64_t tile, int lane, int32_t* s_idx,
                                              float* s_val)
 {
     f4 g[kTileSegs];
     load_tile_grad<FULL>(a, tile, lane, g);
-    const int64_t base = static_cast<int64_t>(a.group_offset[tile / kScanBlock]) + a.tile_offset[tile];
-    scatter_loaded(a, tile, lane, g, base, s_idx, s_val);
+    const uint32_t group_off = a.group_offset[tile / kScanBlock];
+    const uint32_t tile_off = a.tile_offset[tile];
+    const int64_t base = static_cast<int64_t>(group_off) + tile_off;
+    if (EARLY) {
+        uint64_t bw[kTileWords];
+        load_tile_ballots(a, tile, bw);
+        // uses that keep the compiler from sinking these loads to the first
+        // use of each
+#pragma unroll
+        for (int k = 0; k < kTileWords; ++k) asm volatile("" ::"s"(bw[k]));
+        asm volatile("" ::"s"(base));
+        scatter_loaded(a, tile, lane, g, bw, base, s_idx, s_val);
+    } else {
+        scatter_loaded(a, tile, lane, g, a.ballots + tile * kTileWords, base, s_idx, s_val);
+    }
 }
 
-__global__ __launch_bounds__(kSelBlock) void select_scatter(const SelectArgs a0, const SelectBatch bt, bool aligned)
+// 64 VGPRs keep 8 waves per SIMD (the EARLY form needs 71 uncapped).
+template <bool EARLY>
+__global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) void select_scatter(
+    const SelectArgs a0, const SelectBatch bt, bool aligned)
 {
     const SelectArgs a = push_args(a0, bt);
     __shared__ int32_t s_idx[kWavesPerBlock][kStageEntries];
@@ -405,9 +439,9 @@ __global__ __launch_bounds__(kSelBlock) void select_scatter(const SelectArgs a0,
     const int lane = threadIdx.x & (kWave - 1);
     const int w = threadIdx.x / kWave;
     if (aligned && (tile + 1) * kChunksPerTile * 4 <= a.P)
-        scatter_tile<true>(a, tile, lane, s_idx[w], s_val[w]);
+        scatter_tile<true, EARLY>(a, tile, lane, s_idx[w], s_val[w]);
     else
-        scatter_tile<false>(a, tile, lane, s_idx[w], s_val[w]);
+        scatter_tile<false, EARLY>(a, tile, lane, s_idx[w], s_val[w]);
 }
 
 // Two-launch selection, for calls of at most kMaxWideWork blocks of
@@ -468,7 +502,9 @@ __global__ __launch_bounds__(kWideBlock) void select_scatter_wide(const SelectAr
     const int lane = threadIdx.x & (kWave - 1);
     const bool full = aligned && (tile + 1) * kChunksPerTile * 4 <= a.P;
     f4 g[kTileSegs];
+    uint64_t bw[kTileWords];
     if (tile < a.n_tiles) {
+        load_tile_ballots(a, tile, bw);
         if (full)
             load_tile_grad<true>(a, tile, lane, g);
         else
@@ -480,9 +516,8 @@ __global__ __launch_bounds__(kWideBlock) void select_scatter_wide(const SelectAr
     for (int d = kWave / 2; d > 0; d >>= 1) before += __shfl_xor(before, d, kWave);
     uint32_t mine = 0;
     if (tile < a.n_tiles) {
-        const uint64_t* tb = a.ballots + tile * kTileWords;
 #pragma unroll
-        for (int k = 0; k < kTileWords; ++k) mine += __popcll(tb[k]);
+        for (int k = 0; k < kTileWords; ++k) mine += __popcll(bw[k]);
     }
     if (lane == 0) {
         s_before[w] = before;
@@ -496,7 +531,7 @@ __global__ __launch_bounds__(kWideBlock) void select_scatter_wide(const SelectAr
         if (k < w) base += s_tile[k];
     }
     base += block_base;
-    if (tile < a.n_tiles) scatter_loaded(a, tile, lane, g, base, s_idx[w], s_val[w]);
+    if (tile < a.n_tiles) scatter_loaded(a, tile, lane, g, bw, base, s_idx[w], s_val[w]);
     if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) {
         int64_t total = block_base;
 #pragma unroll
@@ -618,7 +653,10 @@ hipError_t launch_select(const SelectArgs& a, const SelectBatch& bt, int B, bool
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    select_scatter<<<grid, kSelBlock, 0, s>>>(a, bt, aligned);
+    if (groups <= static_cast<unsigned>(kFusedTopGroups))
+        select_scatter<true><<<grid, kSelBlock, 0, s>>>(a, bt, aligned);
+    else
+        select_scatter<false><<<grid, kSelBlock, 0, s>>>(a, bt, aligned);
     return hipGetLastError();
 }
 
@@ -640,7 +678,10 @@ hipError_t launch_select_after_mark(const SelectArgs& a, bool aligned, hipStream
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    select_scatter<<<gx, kSelBlock, 0, s>>>(a, bt, aligned);
+    if (groups <= static_cast<unsigned>(kFusedTopGroups))
+        select_scatter<true><<<gx, kSelBlock, 0, s>>>(a, bt, aligned);
+    else
+        select_scatter<false><<<gx, kSelBlock, 0, s>>>(a, bt, aligned);
     return hipGetLastError();
 }
 
