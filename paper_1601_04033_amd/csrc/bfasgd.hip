@@ -164,27 +164,35 @@ __global__ __launch_bounds__(kSelBlock) void select_mark(const SelectArgs a0, co
         mark_tile<false, true>(a, tile, lane);
 }
 
+// Inclusive prefix sum over the wave's 64 lanes in register-to-register
+// DPP adds: row shifts by 1, 2, 4 and 8 give each 16-lane row its own
+// prefix sums (lanes shifted in from outside the row read 0), then the last
+// lane of row 0 is broadcast into row 1 and of row 2 into row 3, and the
+// last lane of row 1 (the sum of lanes 0-31) into rows 2 and 3.
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x)
+{
+    constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0x118;
+    constexpr int kRowBcast15 = 0x142, kRowBcast31 = 0x143;
+    x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), kRowShr1, 0xf, 0xf, false));
+    x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), kRowShr2, 0xf, 0xf, false));
+    x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), kRowShr4, 0xf, 0xf, false));
+    x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), kRowShr8, 0xf, 0xf, false));
+    x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), kRowBcast15, 0xa, 0xf, false));
+    x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), kRowBcast31, 0xc, 0xf, false));
+    return x;
+}
+
 // Block-wide exclusive scan of one value per thread (kScanBlock threads).
 __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* total)
 {
     __shared__ uint32_t wave_total[kScanBlock / kWave];
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
-    uint32_t inc = x;
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        const uint32_t y = __shfl_up(inc, d, kWave);
-        if (lane >= d) inc += y;
-    }
+    const uint32_t inc = wave_inclusive_scan(x);
     if (lane == kWave - 1) wave_total[wave] = inc;
     __syncthreads();
     if (wave == 0) {
-        uint32_t t = lane < kScanBlock / kWave ? wave_total[lane] : 0;
-#pragma unroll
-        for (int d = 1; d < kScanBlock / kWave; d <<= 1) {
-            const uint32_t y = __shfl_up(t, d, kWave);
-            if (lane >= d) t += y;
-        }
+        const uint32_t t = wave_inclusive_scan(lane < kScanBlock / kWave ? wave_total[lane] : 0u);
         if (lane < kScanBlock / kWave) wave_total[lane] = t;
     }
     __syncthreads();
