@@ -22,6 +22,7 @@ import hashlib
 import json
 import os
 import re
+import statistics
 import sys
 import time
 
@@ -162,6 +163,26 @@ def cpu_baseline(pool, theta0_host, clients, ts, c, w, K, P_s):
             "all_cores": {"value": (P_s * K + m) / dt_all, "threads": n_thr, "seconds": dt_all}}
 
 
+GROUPS = 5   # back-to-back groups per figure; the median of their per-call means is reported
+
+
+def grouped_b2b(torch, fn, count, groups=GROUPS):
+    """Per-call ms of `groups` groups of `count` back-to-back calls, each
+    group between two events (after one untimed call): the median of the
+    groups' per-call means, and their range."""
+    fn()
+    means = []
+    for _ in range(groups):
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(count):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        means.append(a.elapsed_time(e) / count)
+    return float(statistics.median(means)), [float(min(means)), float(max(means))]
+
+
 def large_25m(fa, workload, dev, mode, K=32, reps=20):
     """The 25M-parameter workload (50 blocks of 500k, lambda = 64) beside the
     main one: the dense pass at K = 1, 8, 32, the server's step (one
@@ -179,7 +200,7 @@ def large_25m(fa, workload, dev, mode, K=32, reps=20):
     theta.copy_(theta0)
     del theta0
     st = fa.fasgd_init_state(theta, n, b, v, last_T, lam=w.lam, alpha=w.alpha_fasgd, math_mode=mode)
-    clients, ts = workload.schedule(w, K + 11 * (1 + 8 + 32) + (2 * reps + 4) * (K + 1) + 64)
+    clients, ts = workload.schedule(w, K + (GROUPS * 10 + 1) * (1 + 8 + 32) + (GROUPS * reps + 4) * (K + 1) + 64)
     idx = torch.empty(P, device=dev, dtype=torch.int32)
     val = torch.empty(P, device=dev)
     cnt = torch.zeros(1, device=dev, dtype=torch.int64)
@@ -190,22 +211,16 @@ def large_25m(fa, workload, dev, mode, K=32, reps=20):
     c = calibrate_c(v, w.transmit_fraction or 0.1)
 
     def b2b(fn, count):
-        fn()
-        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        for _ in range(count):
-            fn()
-        e.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(e) / count
+        return grouped_b2b(torch, fn, count)
 
     out = {"P": P, "lambda": w.lam, "dense": {}}
     for k in (1, 8, 32):
         def dense(k=k):
             T = st.T
             fa.fasgd_apply_updates(st, pool[:k], clients[T:T + k], ts[T:T + k])
-        ms = b2b(dense, 10)
-        out["dense"][f"K={k}"] = {"ms": ms, "frac": P * (32 + 4 * k) / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+        ms, spread = b2b(dense, 10)
+        out["dense"][f"K={k}"] = {"ms": ms, "frac": P * (32 + 4 * k) / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                                  "ms_range": spread}
     # the server's step, its pass timed alone with events around the kernel
     T = st.T
     fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, T, clients[T], idx, val, cnt, ws, seg_start=seg)
@@ -219,20 +234,21 @@ def large_25m(fa, workload, dev, mode, K=32, reps=20):
                                             clients[T + 1:T + 1 + K], ts[T + 1:T + 1 + K], pool[K],
                                             clients[T + K + 1], c, EPS_C, SEED, idx, val, cnt, seg, ws)
         passes.append((p0, p1))
-    step_ms = b2b(step, reps)
+    step_ms, step_spread = b2b(step, reps)
     torch.cuda.synchronize()
     pass_ms = sum(a.elapsed_time(e) for a, e in passes[1:]) / len(passes[1:])
     m = int(cnt.item())
     pass_bytes = P * (32 + 4 * K) + 8 * m + 4 * fa.bfasgd_list_index_length(P) + P / 8
-    out["step"] = {"ms": step_ms, "param_updates_per_s": (P * K + m) / (step_ms * 1e-3),
+    out["step"] = {"ms": step_ms, "ms_range": step_spread, "param_updates_per_s": (P * K + m) / (step_ms * 1e-3),
                    "pass_ms": pass_ms, "pass_frac": pass_bytes / (pass_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
                    "transmitted_fraction": m / P}
     T = st.T
     fa.bfasgd_apply_sparse(st, idx, val, cnt, clients[T], ts[T])
-    sel_ms = b2b(lambda: fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, st.T, clients[st.T], idx, val, cnt,
-                                                  ws), reps)
+    sel_ms, sel_spread = b2b(lambda: fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, st.T, clients[st.T], idx,
+                                                              val, cnt, ws), reps)
     m = int(cnt.item())
-    out["bfasgd_select_compact"] = {"ms": sel_ms, "frac": (8 * P + 8 * m) / (sel_ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+    out["bfasgd_select_compact"] = {"ms": sel_ms, "frac": (8 * P + 8 * m) / (sel_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                                    "ms_range": sel_spread}
     return out
 
 
@@ -431,7 +447,8 @@ def main():
     # pushes, 3 synchronous steps and the dense passes at K = 1, 8, 32 (11
     # calls each)
     KS = (1, 8, 32)
-    clients, ts = workload.schedule(w, K + (warm + steps + 6) * per_step + 2 + 3 * K + 9 + 16 + 11 * sum(KS))
+    clients, ts = workload.schedule(w, K + (warm + steps + 6) * per_step + 2 + 3 * K + 9 + 16
+                                    + (GROUPS * 10 + 1) * sum(KS))
     torch.cuda.synchronize()
 
     # One step: one call (fasgd_apply_with_push_and_select) whose pass
@@ -586,21 +603,14 @@ def main():
     sas_bytes = P * (8 + 4 * K)
 
     def batch_ms(fn, n):
-        """Per-call ms of n back-to-back calls between two events (after one
-        untimed call): the rate the kernels sustain, without per-call event
-        and dispatch gaps."""
-        fn()
-        a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        for _ in range(n):
-            fn()
-        b_.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(b_) / n
+        """Per-call ms of back-to-back calls (the median over groups of n
+        calls between two events): the rate the kernels sustain, without
+        per-call event and dispatch gaps."""
+        return grouped_b2b(torch, fn, n)
 
     # the push selection back to back on the step's last inputs
-    sel_b2b_ms = batch_ms(lambda: fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, st.T, clients[st.T],
-                                                          idx, val, cnt, ws), 20)
+    sel_b2b_ms, sel_b2b_range = batch_ms(lambda: fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, st.T,
+                                                                          clients[st.T], idx, val, cnt, ws), 20)
     m_b2b = int(cnt.item())
     sel_b2b_bytes = P * 8 + m_b2b * 8
     # the dense pass at K = 1, 8, 32 (gradients fused per pass), back to back
@@ -609,8 +619,8 @@ def main():
         def dense_pass(k=k):
             base = st.T
             fa.fasgd_apply_updates(st, pool[:k], clients[base:base + k], ts[base:base + k])
-        kms = batch_ms(dense_pass, 10)
-        dense_k[str(k)] = {"ms": kms, "GB/s": P * (32 + 4 * k) / (kms * 1e-3) / 1e9,
+        kms, krange = batch_ms(dense_pass, 10)
+        dense_k[str(k)] = {"ms": kms, "ms_range": krange, "GB/s": P * (32 + 4 * k) / (kms * 1e-3) / 1e9,
                            "frac": P * (32 + 4 * k) / (kms * 1e-3) / 1e9 / HBM_PEAK_GBS,
                            "param_updates_per_s": P * k / (kms * 1e-3)}
 
@@ -718,7 +728,7 @@ def main():
                                     "back_to_back_by_K": dense_k},
             "step_as_separate_calls": {"ms": sep_ms_avg,
                                        "calls": "fasgd_apply_updates, bfasgd_select_compact, bfasgd_apply_sparse"},
-            "bfasgd_select_compact": {"ms_back_to_back": sel_b2b_ms,
+            "bfasgd_select_compact": {"ms_back_to_back": sel_b2b_ms, "ms_back_to_back_range": sel_b2b_range,
                                       "GB/s_back_to_back": sel_b2b_bytes / (sel_b2b_ms * 1e-3) / 1e9,
                                       "frac_back_to_back": sel_b2b_bytes / (sel_b2b_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
                                       "transmitted_fraction": m_avg / P},
