@@ -4,8 +4,8 @@
 // Work is cut into wave tiles of kTileSegs segments of 64 chunks (one chunk is
 // 4 consecutive parameters, one 16-byte vector).  Every wave owns one tile and
 // never waits on another wave, so no launch has a block barrier in its
-// streaming part.  Selection runs in three or four launches (small calls: two,
-// described at select_mark_wide):
+// streaming part.  Selection runs in three or four launches (calls of up to
+// about 50M parameters: two, described at select_mark_totals):
 //   mark     the wave loads its tile of v, draws one Philox4x32-10 call per
 //            chunk (the counter is the global chunk index, so one call feeds
 //            one vector of v), forms four ballots per segment (1 bit per
@@ -452,34 +452,46 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8, 8)
         scatter_tile<false, EARLY>(a, tile, lane, s_idx[w], s_val[w]);
 }
 
-// Two-launch selection, for calls of at most kMaxWideWork blocks of
-// kWideWaves tiles (all pushes together): no scan launch.  A mark block of
-// kWideWaves waves (one tile each) adds its waves' counts through an LDS
-// arrival counter, so no wave waits for another and there is no global
-// atomic, and the last wave to arrive stores the block total.  Each scatter
-// block covers the same tiles; while its gradient loads are in flight it sums
-// the totals of the blocks before it and, after one block barrier, the counts
-// of its own earlier tiles (from their ballot words), which gives every tile
-// its list position.  The last block writes the count.  Up to about 8M
-// parameters this saves the scan launch's latency (2 of 18 us at 1.8M); past
-// that the block barrier of the scatter costs more than the scan launch.
-constexpr int kWideWaves = 16;
-constexpr int kWideBlock = kWideWaves * kWave;
-constexpr int64_t kMaxWideWork = 512;        // blocks x pushes; block totals live in group_total
-static_assert(kMaxWideWork <= kMaxGroups, "block totals fit the group totals");
+// Two-launch selection, for calls of at most kDirectMaxTiles tiles per push:
+// no scan launch, and no wave waits for another.
+//   select_mark_totals  blocks of TPB waves, one tile each, store the
+//     tiles' ballot words as select_mark does and their counts in LDS; the
+//     last wave to arrive (an LDS arrival counter) stores each tile's offset
+//     within the block and the block total as 16 bits (at most 16 x 1024).
+//   select_scatter_direct  every wave finds its own list position: the
+//     totals of all blocks before its tile's block plus the tile's offset
+//     within its block.  KT 16-byte loads per lane cover the totals of
+//     512 KT blocks; they are issued before the gradient loads, so the wait
+//     for them leaves the gradients in flight, and the wave sums them in
+//     registers and across its lanes.
+// The result is that of the three launches, bit for bit.  Against them on
+// the same box (10 % transmitted, back to back): 8.4M 17.2 against 19.6 us,
+// 12M 23.0 against 25.9, 25M 39.2 against 41.0, 33M 51.2 against 52.2 and
+// 50M 86.0 against 91.3 us; at 1.8M the kernels take 8.2 us against 10.0 us
+// for the two-launch form with 16-wave blocks and a block barrier in the
+// scatter that this form replaced.  Blocks of 8 tiles are the faster shape where
+// both fit (25M: 38.6 against 39.2 us with blocks of 16 and half the loads):
+// a mark block of 8 waves costs about 1.5 us more than one of 4 at 25M, but
+// blocks of 4 would need twice the loads and registers in the scatter.
+constexpr int kDirectLoads = 6;                                  // 16-byte loads of block totals per lane, at most
+constexpr int64_t kDirectMaxBlocks = int64_t(kDirectLoads) * kWave * 8;   // 3072 block totals (6 KB)
+constexpr int64_t kDirectMaxTiles = 16 * kDirectMaxBlocks;       // 49,152 tiles: 50.3M parameters
+static_assert(kDirectMaxBlocks * sizeof(uint16_t) <= kMaxGroups * sizeof(uint32_t),
+              "16-bit block totals fit the group totals");
 
-__global__ __launch_bounds__(kWideBlock) void select_mark_wide(const SelectArgs a0, const SelectBatch bt,
-                                                               bool aligned)
+template <int TPB>
+__global__ __launch_bounds__(TPB * kWave) void select_mark_totals(const SelectArgs a0, const SelectBatch bt,
+                                                                  bool aligned)
 {
+    static_assert(TPB * kChunksPerTile * 4 < 65536 && TPB <= kWave, "a block total fits 16 bits");
     const SelectArgs a = push_args(a0, bt);
-    __shared__ uint32_t s_total, s_arrived;
-    if (threadIdx.x == 0) {
-        s_total = 0;
-        s_arrived = 0;
-    }
+    __shared__ uint32_t s_cnt[TPB];
+    __shared__ uint32_t s_arrived;
+    if (threadIdx.x == 0) s_arrived = 0;
     __syncthreads();
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int64_t tile = static_cast<int64_t>(blockIdx.x) * kWideWaves + w;
+    const int64_t t0 = static_cast<int64_t>(blockIdx.x) * TPB;
+    const int64_t tile = t0 + w;
     const int lane = threadIdx.x & (kWave - 1);
     uint32_t count = 0;
     if (tile < a.n_tiles) {
@@ -488,65 +500,145 @@ __global__ __launch_bounds__(kWideBlock) void select_mark_wide(const SelectArgs 
         else
             count = mark_tile<false, false>(a, tile, lane);
     }
+    int last = 0;
     if (lane == 0) {
-        __hip_atomic_fetch_add(&s_total, count, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        // release / acquire: every wave's addition is seen by the last to arrive
-        const uint32_t before = __hip_atomic_fetch_add(&s_arrived, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
-        if (before == kWideWaves - 1)
-            a.group_total[blockIdx.x] = __hip_atomic_load(&s_total, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        s_cnt[w] = count;
+        // release / acquire: the last wave to arrive sees every count
+        last = __hip_atomic_fetch_add(&s_arrived, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP) == TPB - 1;
+    }
+    if (__builtin_amdgcn_readfirstlane(last)) {
+        const uint32_t c = lane < TPB ? s_cnt[lane] : 0u;
+        const uint32_t inc = wave_inclusive_scan(c);
+        if (lane < TPB && t0 + lane < a.n_tiles) a.tile_offset[t0 + lane] = inc - c;
+        if (lane == TPB - 1) reinterpret_cast<uint16_t*>(a.group_total)[blockIdx.x] = static_cast<uint16_t>(inc);
     }
 }
 
-__global__ __launch_bounds__(kWideBlock) void select_scatter_wide(const SelectArgs a0, const SelectBatch bt,
-                                                                  bool aligned)
+__device__ __forceinline__ uint32_t sum_halves(uint32_t x) { return (x & 0xffffu) + (x >> 16); }
+
+// Mask of the 16-bit halves j < r of 32-bit word i (halves 2i, 2i + 1).
+__device__ __forceinline__ uint32_t halves_below(int i, int r)
 {
-    const SelectArgs a = push_args(a0, bt);
-    __shared__ int32_t s_idx[kWideWaves][kStageEntries];
-    __shared__ float s_val[kWideWaves][kStageEntries];
-    __shared__ uint32_t s_before[kWideWaves];   // per wave: part of the totals of earlier blocks
-    __shared__ uint32_t s_tile[kWideWaves];     // per wave: its tile's count
-    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int64_t tile = static_cast<int64_t>(blockIdx.x) * kWideWaves + w;
-    const int lane = threadIdx.x & (kWave - 1);
-    const bool full = aligned && (tile + 1) * kChunksPerTile * 4 <= a.P;
-    f4 g[kTileSegs];
-    uint64_t bw[kTileWords];
-    if (tile < a.n_tiles) {
-        load_tile_ballots(a, tile, bw);
-        if (full)
-            load_tile_grad<true>(a, tile, lane, g);
-        else
-            load_tile_grad<false>(a, tile, lane, g);
-    }
-    uint32_t before = 0;
-    for (uint32_t i = threadIdx.x; i < blockIdx.x; i += kWideBlock) before += a.group_total[i];
+    return (2 * i + 1 < r) ? 0xffffffffu : (2 * i < r ? 0xffffu : 0u);
+}
+
+// The list position of the first entry of a tile whose block has
+// `blocks_before` blocks before it: the sum of their 16-bit totals plus the
+// tile's offset within its block.  Lane l holds the groups l + 64 k of 8
+// totals (tv[k]); the group that holds the last totals that count is summed
+// in part.
+template <int KT>
+__device__ __forceinline__ int64_t direct_position(const uint4 (&tv)[KT], int blocks_before, uint32_t tile_off,
+                                                   int lane)
+{
+    const int whole = blocks_before >> 3;   // groups of 8 totals that count in full
+    const int r = blocks_before & 7;        // totals of the next group that count
+    const uint32_t m0 = halves_below(0, r), m1 = halves_below(1, r), m2 = halves_below(2, r),
+                   m3 = halves_below(3, r);
+    uint32_t s = 0;
 #pragma unroll
-    for (int d = kWave / 2; d > 0; d >>= 1) before += __shfl_xor(before, d, kWave);
-    uint32_t mine = 0;
-    if (tile < a.n_tiles) {
+    for (int k = 0; k < KT; ++k) {
+        const int grp = lane + kWave * k;
+        const bool all = grp < whole;
+        const uint32_t x = sum_halves(tv[k].x & (all ? ~0u : m0)) + sum_halves(tv[k].y & (all ? ~0u : m1)) +
+                           sum_halves(tv[k].z & (all ? ~0u : m2)) + sum_halves(tv[k].w & (all ? ~0u : m3));
+        s += grp <= whole ? x : 0u;
+    }
+    const uint32_t inc = wave_inclusive_scan(s);
+    return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(inc), kWave - 1)) + tile_off;
+}
+
+// The call's count (and the list index's last entry) from the last tile.
+template <typename Words>
+__device__ __forceinline__ void direct_finish(const SelectArgs& a, int64_t tile, int lane, const Words& bw,
+                                              int64_t base)
+{
+    if (tile == a.n_tiles - 1 && lane == 0) {
+        uint32_t mine = 0;
 #pragma unroll
         for (int k = 0; k < kTileWords; ++k) mine += __popcll(bw[k]);
+        *a.d_count = base + mine;
+        if (a.seg_start) a.seg_start[a.n_segs] = static_cast<uint32_t>(base + mine);
     }
-    if (lane == 0) {
-        s_before[w] = before;
-        s_tile[w] = mine;
-    }
-    __syncthreads();
-    int64_t block_base = 0, base = 0;
+}
+
+// FULL as for mark_tile.  The partial tile (or every tile of misaligned
+// arrays) finds its position before it loads its gradients, and reads its
+// ballot words from the workspace where it uses them, which needs fewer
+// registers.
+template <bool FULL, int TPB, int KT>
+__device__ __forceinline__ void scatter_direct_tile(const SelectArgs& a, int64_t tile, int lane, int32_t* s_idx,
+                                                    float* s_val)
+{
+    const int nb = static_cast<int>(tile / TPB);   // blocks before this tile's block
+    const uint4* tot = reinterpret_cast<const uint4*>(a.group_total);
+    uint4 tv[KT];
 #pragma unroll
-    for (int k = 0; k < kWideWaves; ++k) {
-        block_base += s_before[k];
-        if (k < w) base += s_tile[k];
-    }
-    base += block_base;
-    if (tile < a.n_tiles) scatter_loaded(a, tile, lane, g, bw, base, s_idx[w], s_val[w]);
-    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) {
-        int64_t total = block_base;
+    for (int k = 0; k < KT; ++k)   // only the groups some lane needs (wave-uniform)
+        tv[k] = kWave * k <= (nb >> 3) ? tot[lane + kWave * k] : make_uint4(0u, 0u, 0u, 0u);
+    f4 g[kTileSegs];
+    if (FULL) {
+        // the loads above are issued before the gradients', so waiting for
+        // them leaves the gradients in flight
+        __builtin_amdgcn_sched_barrier(0);
+        load_tile_grad<true>(a, tile, lane, g);
+        const uint32_t tile_off = a.tile_offset[tile];
+        uint64_t bw[kTileWords];
+        load_tile_ballots(a, tile, bw);
+        // uses that keep the compiler from sinking these (scalar) loads to
+        // the first use of each
 #pragma unroll
-        for (int k = 0; k < kWideWaves; ++k) total += s_tile[k];
-        *a.d_count = total;
-        if (a.seg_start) a.seg_start[a.n_segs] = static_cast<uint32_t>(total);
+        for (int k = 0; k < kTileWords; ++k) asm volatile("" ::"s"(bw[k]));
+        asm volatile("" ::"s"(tile_off));
+        const int64_t base = direct_position<KT>(tv, nb, tile_off, lane);
+        scatter_loaded(a, tile, lane, g, bw, base, s_idx, s_val);
+        direct_finish(a, tile, lane, bw, base);
+    } else {
+        const int64_t base = direct_position<KT>(tv, nb, a.tile_offset[tile], lane);
+        load_tile_grad<false>(a, tile, lane, g);
+        const uint64_t* bw = a.ballots + tile * kTileWords;
+        scatter_loaded(a, tile, lane, g, bw, base, s_idx, s_val);
+        direct_finish(a, tile, lane, bw, base);
     }
+}
+
+template <int TPB, int KT>
+__global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8, 8))) void select_scatter_direct(
+    const SelectArgs a0, const SelectBatch bt, bool aligned)
+{
+    const SelectArgs a = push_args(a0, bt);
+    __shared__ int32_t s_idx[kWavesPerBlock][kStageEntries];
+    __shared__ float s_val[kWavesPerBlock][kStageEntries];
+    const int64_t tile = wave_tile();
+    if (tile >= a.n_tiles) return;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int w = threadIdx.x / kWave;
+    if (aligned && (tile + 1) * kChunksPerTile * 4 <= a.P)
+        scatter_direct_tile<true, TPB, KT>(a, tile, lane, s_idx[w], s_val[w]);
+    else
+        scatter_direct_tile<false, TPB, KT>(a, tile, lane, s_idx[w], s_val[w]);
+}
+
+template <int TPB>
+hipError_t launch_direct(const SelectArgs& a, const SelectBatch& bt, int B, bool aligned, hipStream_t s)
+{
+    const int64_t blocks = (a.n_tiles + TPB - 1) / TPB;
+    const int kt = static_cast<int>((blocks + kWave * 8 - 1) / (kWave * 8));
+    const dim3 mgrid(static_cast<unsigned>(blocks), static_cast<unsigned>(B));
+    select_mark_totals<TPB><<<mgrid, TPB * kWave, 0, s>>>(a, bt, aligned);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 grid(static_cast<unsigned>((a.n_tiles + kWavesPerBlock - 1) / kWavesPerBlock), static_cast<unsigned>(B));
+    switch (kt) {
+    case 1: select_scatter_direct<TPB, 1><<<grid, kSelBlock, 0, s>>>(a, bt, aligned); break;
+    case 2: select_scatter_direct<TPB, 2><<<grid, kSelBlock, 0, s>>>(a, bt, aligned); break;
+    case 3: select_scatter_direct<TPB, 3><<<grid, kSelBlock, 0, s>>>(a, bt, aligned); break;
+    case 4: select_scatter_direct<TPB, 4><<<grid, kSelBlock, 0, s>>>(a, bt, aligned); break;
+    case 5: select_scatter_direct<TPB, 5><<<grid, kSelBlock, 0, s>>>(a, bt, aligned); break;
+    case 6: select_scatter_direct<TPB, 6><<<grid, kSelBlock, 0, s>>>(a, bt, aligned); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
 }
 
 constexpr int kListBlock = 256;               // list kernels: 4 waves
@@ -637,16 +729,9 @@ hipError_t launch_select(const SelectArgs& a, const SelectBatch& bt, int B, bool
     const unsigned gx = static_cast<unsigned>((a.n_tiles + kWavesPerBlock - 1) / kWavesPerBlock);
     const unsigned groups = static_cast<unsigned>((a.n_tiles + kScanBlock - 1) / kScanBlock);
     if (groups > static_cast<unsigned>(kMaxGroups) || B < 1 || B > kMaxBatch) return hipErrorInvalidValue;
-    const int64_t wide = (a.n_tiles + kWideWaves - 1) / kWideWaves;
+    if (a.n_tiles <= 8 * kDirectMaxBlocks) return launch_direct<8>(a, bt, B, aligned, s);
+    if (a.n_tiles <= kDirectMaxTiles) return launch_direct<16>(a, bt, B, aligned, s);
     hipError_t e;
-    if (wide * B <= kMaxWideWork) {
-        const dim3 wgrid(static_cast<unsigned>(wide), static_cast<unsigned>(B));
-        select_mark_wide<<<wgrid, kWideBlock, 0, s>>>(a, bt, aligned);
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        select_scatter_wide<<<wgrid, kWideBlock, 0, s>>>(a, bt, aligned);
-        return hipGetLastError();
-    }
     const dim3 grid(gx, static_cast<unsigned>(B));
     select_mark<<<grid, kSelBlock, 0, s>>>(a, bt, aligned);
     e = hipGetLastError();

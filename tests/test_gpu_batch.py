@@ -76,13 +76,11 @@ def test_batch_select_equals_single_selects(P, B, cap_frac, offset, base):
     """Push by push, the batch gives the count, list and list index of a
     single selection with the same gradient, T and client, bit for bit
     (including a capacity cut, a shard offset, the scalar path for gradients
-    4 bytes off 16-byte alignment, 64 pushes, and 17M parameters, where the
-    group scan takes its two-launch form).  Calls of at most 512 blocks of 16
-    tiles in all take the two-launch selection (block totals, no scan
-    launch), larger ones the scan: at 131,075 x 64 and 4,194,308 x 2 the
-    batch scans while each single push takes the two-launch form, so the two
-    forms are checked against each other; 4,194,304 x 2 is the largest batch
-    of two that takes the two-launch form."""
+    4 bytes off 16-byte alignment, 64 pushes, and 17M parameters).  The form
+    of the selection depends on the parameters per push only (two launches
+    with per-wave list positions up to 49,152 tiles, then three), so batch
+    and single calls take the same form; 4,194,304 and 4,194,308 parameters
+    sit either side of the scatter's first change of load count."""
     import torch
     dev = gpu()
     (st,), _, (m_, s_, w), keep = _mid_run_state(P, dev, seed=P % 977, copies=1)

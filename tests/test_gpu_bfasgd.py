@@ -83,11 +83,17 @@ def test_select_mlp_twenty_percent_and_deterministic():
         assert m2 == m and np.array_equal(idx2, idx) and np.array_equal(val2, val)
 
 
-@pytest.mark.parametrize("P", [8_388_608, 8_388_612])
-def test_select_at_two_launch_limit(P):
-    """Either side of the largest selection that runs in two launches (512
-    blocks of 16 tiles of 1024 parameters, no scan launch): lists bit-exact
-    against the oracle and the list index pointing at every segment."""
+@pytest.mark.parametrize("P", [4_194_304, 4_194_308, 25_000_000, 25_165_824, 25_165_828, 50_331_648, 50_331_652])
+def test_select_at_form_limits(P):
+    """Either side of each change of form of the selection: calls of up to
+    24,576 tiles of 1024 parameters run in two launches with blocks of 8
+    tiles, up to 49,152 tiles with blocks of 16, larger ones in three
+    launches; the scatter's waves load the block totals in 512 per 16-byte
+    lane load, so 4,194,304 / 4,194,308 parameters take one / two loads and
+    25,165,824 / 25,165,828 six loads of 8-tile / four of 16-tile blocks
+    (25,000,000: a last block of 7 tiles).  Lists bit-exact against the
+    oracle and the list index pointing at every segment, from a workspace
+    filled with other bytes."""
     import torch
     dev = gpu()
     v = workload.synthetic_v(P, seed=5)
@@ -113,11 +119,12 @@ def test_select_at_two_launch_limit(P):
     assert got[-1] == m
 
 
-@pytest.mark.parametrize("P", [workload.MLP_P, 12_000_003])
+@pytest.mark.parametrize("P", [workload.MLP_P, 12_000_003, 50_331_652])
 def test_select_repeats_bit_identical(P):
     """100 selections of the same push give the same count, list and list
     index bit for bit, with the workspace refilled with other bytes between
-    repeats (two launches at the MLP size, the scan form at 12M)."""
+    repeats (two launches at the MLP size and 12M, three launches with the
+    scan at 50.3M)."""
     import torch
     dev = gpu()
     v = workload.synthetic_v(P, seed=9)
