@@ -405,9 +405,10 @@ __device__ __forceinline__ void scatter_loaded(const SelectArgs& a, int64_t tile
 
 // EARLY: every ballot word and the list position are loaded and waited for
 // while the gradient loads are in flight.  In calls of at most
-// kFusedTopGroups groups (up to 67M parameters) every wave's latency is
-// exposed, and this took the 25M selection from 44.0-46.6 to 41.5-45.1 us
-// (same box, lists identical).  Otherwise the compiler issues each part
+// kFusedTopGroups groups (up to 67M parameters: the scan after a pass that
+// took the decisions, and standalone calls past the two-launch form) every
+// wave's latency is exposed, and this took the 25M selection, then in three
+// launches, from 44.0-46.6 to 41.5-45.1 us (same box, lists identical).  Otherwise the compiler issues each part
 // where it is first used (three dependent scalar round trips per tile),
 // which was 3 % faster at 1e9 (1.63-1.65 against 1.70 ms), where many more
 // waves are in flight to cover them.
