@@ -470,10 +470,11 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8, 8)
 // 12M 23.0 against 25.9, 25M 39.2 against 41.0, 33M 51.2 against 52.2 and
 // 50M 86.0 against 91.3 us; at 1.8M the kernels take 8.2 us against 10.0 us
 // for the two-launch form with 16-wave blocks and a block barrier in the
-// scatter that this form replaced.  Blocks of 8 tiles are the faster shape where
-// both fit (25M: 38.6 against 39.2 us with blocks of 16 and half the loads):
-// a mark block of 8 waves costs about 1.5 us more than one of 4 at 25M, but
-// blocks of 4 would need twice the loads and registers in the scatter.
+// scatter that this form replaced.  Blocks of 8 tiles are the faster shape
+// where both fit (probes at 25M: 38.6 against 39.2 us with blocks of 16 and
+// half the loads).  A mark block of 8 waves takes 1.1-1.4 us longer than one
+// of 4 at 25M (it needs 8 free wave slots on a CU to start), but blocks of 4
+// would need twice the loads and more registers than the scatter has.
 constexpr int kDirectLoads = 6;                                  // 16-byte loads of block totals per lane, at most
 constexpr int64_t kDirectMaxBlocks = int64_t(kDirectLoads) * kWave * 8;   // 3072 block totals (6 KB)
 constexpr int64_t kDirectMaxTiles = 16 * kDirectMaxBlocks;       // 49,152 tiles: 50.3M parameters

@@ -72,7 +72,7 @@ def _batch_buffers(B, P, cap, dev):
     (1, 3, 1.0, 0, 0), (1027, 16, 1.0, 0, 0), (100_003, 16, 1.0, 0, 0), (100_003, 5, 0.05, 0, 0),
     (100_003, 6, 1.0, 0, 4 * 123_457), (1_000_003, 64, 1.0, 0, 0), (65_537, 7, 1.0, 1, 0),
     (17_000_003, 3, 1.0, 0, 0), (131_075, 64, 1.0, 0, 0), (4_194_308, 2, 0.5, 0, 0), (4_194_304, 2, 1.0, 1, 0),
-    (50_331_652, 2, 1.0, 0, 0)])
+    (30_000_001, 2, 0.5, 1, 0), (50_331_652, 2, 1.0, 0, 0)])
 def test_batch_select_equals_single_selects(P, B, cap_frac, offset, base):
     """Push by push, the batch gives the count, list and list index of a
     single selection with the same gradient, T and client, bit for bit
@@ -81,8 +81,10 @@ def test_batch_select_equals_single_selects(P, B, cap_frac, offset, base):
     of the selection depends on the parameters per push only (two launches
     with per-wave list positions up to 49,152 tiles, then three), so batch
     and single calls take the same form; 4,194,304 and 4,194,308 parameters
-    sit either side of the scatter's first change of load count, and
-    50,331,652 is the smallest size the three launches take."""
+    sit either side of the scatter's first change of load count,
+    30,000,001 takes blocks of 16 tiles (with misaligned gradients and a
+    capacity cut), and 50,331,652 is the smallest size the three launches
+    take."""
     import torch
     dev = gpu()
     (st,), _, (m_, s_, w), keep = _mid_run_state(P, dev, seed=P % 977, copies=1)

@@ -191,6 +191,39 @@ def test_select_misaligned_views():
     np.testing.assert_array_equal(val.view(np.uint32), r_val.view(np.uint32))
 
 
+def test_select_sixteen_tile_blocks_misaligned_with_capacity_cut():
+    """The two-launch form with blocks of 16 tiles (30M parameters) with v and
+    the gradient 4 bytes off 16-byte alignment, so that every tile sums the
+    block totals before it loads its gradients, and a capacity of half the
+    count: the count is the full m, the first entries are the oracle's bit
+    for bit, and nothing is written past the capacity."""
+    import torch
+    dev = gpu()
+    P = 30_000_001
+    v = workload.synthetic_v(P, seed=8)
+    g = np.random.default_rng(8).standard_normal(P).astype(np.float32)
+    st = new_gpu_state(np.zeros(P, np.float32), dev, 4, 0.005, fa.MATH_FAST)
+    vb = torch.empty(P + 1, device=dev)
+    vb[1:].copy_(torch.from_numpy(v))
+    st.c.v = vb[1:].data_ptr()
+    st.tensors["v"] = vb[1:]
+    gb = torch.empty(P + 1, device=dev)
+    gb[1:].copy_(torch.from_numpy(g))
+    r_idx, r_val, r_m = oracle.bfasgd_select(v, g, 40.0, 1e-8, SEED, 13, 3)
+    cap = r_m // 2
+    idx = torch.full((cap + 1000,), -7, device=dev, dtype=torch.int32)
+    val = torch.zeros(cap + 1000, device=dev)
+    cnt = torch.full((1,), -1, device=dev, dtype=torch.int64)
+    ws = fa.allocate_workspace(P, dev)
+    ws.fill_(0xC3)
+    fa.bfasgd_select_compact(st, gb[1:], 40.0, 1e-8, SEED, 13, 3, idx[:cap], val[:cap], cnt, ws)
+    torch.cuda.synchronize()
+    assert int(cnt.item()) == r_m
+    np.testing.assert_array_equal(idx[:cap].cpu().numpy(), r_idx[:cap])
+    np.testing.assert_array_equal(val[:cap].cpu().numpy().view(np.uint32), r_val[:cap].view(np.uint32))
+    assert (idx[cap:] == -7).all() and (val[cap:] == 0).all()
+
+
 @pytest.mark.parametrize("mode", [fa.MATH_FAST, fa.MATH_IEEE])
 def test_sparse_apply_matches_oracle_and_transmit_all_is_dense(mode):
     import torch
