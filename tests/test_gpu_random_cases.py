@@ -3,7 +3,8 @@ fixed seed per case (sizes with ragged tails and sizes next to the vector,
 segment and tile edges; thresholds, keys, shard offsets, capacity cuts and
 misaligned views; both math modes and both readings of v; random K and
 staleness), each held to the same bar as the enumerated tests:
- * the selection against the oracle, bit-exact, with the list index;
+ * the selection against the oracle, bit-exact, with the list index (also
+   at sizes from 5M to 54M, one per form of the selection);
  * a K-update sequence against the oracle within the sequence tolerance;
  * the push applied inside the pass, and the server's step that also takes
    the next push's decisions, bit-identical to the separate calls;
@@ -46,10 +47,29 @@ def _offset_view(host, dev, off):
 
 @pytest.mark.parametrize("case", range(N_CASES))
 def test_random_selection_matches_oracle(case):
-    import torch
     rng = np.random.default_rng(1000 + case)
+    _random_selection(rng, case, _size(rng, 3_000_000))
+
+
+# one size near the middle of each load count of the two-launch form's
+# scatter (2 to 6 loads with blocks of 8 tiles, 4 to 6 with blocks of 16)
+# and one past it (three launches), jittered by up to 1M with a ragged tail
+LARGE_SIZES = (6_300_000, 10_500_000, 14_700_000, 18_900_000, 23_100_000, 29_000_000, 37_700_000, 46_000_000,
+               53_000_000)
+
+
+@pytest.mark.parametrize("case", range(len(LARGE_SIZES)))
+def test_random_large_selection_matches_oracle(case):
+    """Every form of the selection from 4.2M to 55M parameters, to the same
+    bar as the small random cases."""
+    rng = np.random.default_rng(5000 + case)
+    P = LARGE_SIZES[case] + int(rng.integers(-1_000_000, 1_000_000))
+    _random_selection(rng, 100 + case, P)
+
+
+def _random_selection(rng, case, P):
+    import torch
     dev = gpu()
-    P = _size(rng, 3_000_000)
     v = workload.synthetic_v(P, seed=case, lo=float(rng.uniform(0.1, 10)), hi=float(rng.uniform(20, 400)))
     g = rng.standard_normal(P).astype(np.float32)
     c = float(np.float32(np.exp(rng.uniform(np.log(0.05), np.log(5e3)))))
