@@ -56,3 +56,35 @@ def test_fetch_copy_rule_follows_the_header():
     assert bench.fetch_copy_by_segments(P, P // 10)
     assert not bench.fetch_copy_by_segments(P, P // 100)
     assert not bench.fetch_copy_by_segments(25_000_000, 2_500_000)
+
+
+def test_grouped_timing_reports_the_median_group():
+    """Back-to-back figures: one untimed call, then five groups of n calls
+    between two events each; the per-call median of the groups and their
+    range.  A clock that advances 1 per event and 0.5 per call, with one slow
+    group, stands in for the GPU."""
+    import types
+
+    class Event:
+        now = 0.0
+
+        def __init__(self, enable_timing=True):
+            self.at = None
+
+        def record(self):
+            Event.now += 1.0
+            self.at = Event.now
+
+        def elapsed_time(self, end):
+            return end.at - self.at
+
+    calls = [0]
+
+    def fn():
+        calls[0] += 1
+        Event.now += 0.5 if calls[0] != 30 else 100.5     # call 30 falls in the third group
+
+    fake = types.SimpleNamespace(cuda=types.SimpleNamespace(Event=Event, synchronize=lambda: None))
+    ms, (lo, hi) = bench.grouped_b2b(fake, fn, 10)
+    assert calls[0] == 1 + 5 * 10
+    assert ms == pytest.approx(0.6) and lo == pytest.approx(0.6) and hi == pytest.approx(10.6)
