@@ -18,6 +18,7 @@ timed after the step, cover the other entry points and the small workloads
 handled one by one or in batches), eagerly and as replayed HIP graphs.
 """
 import argparse
+import ctypes
 import hashlib
 import json
 import os
@@ -163,6 +164,55 @@ def cpu_baseline(pool, theta0_host, clients, ts, c, w, K, P_s):
             "all_cores": {"value": (P_s * K + m) / dt_all, "threads": n_thr, "seconds": dt_all}}
 
 
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000   # hipEventDisableSystemFence
+
+
+class TimingEvent:
+    """A HIP event for timing only, created with hipEventDisableSystemFence:
+    recording it writes a timestamp without the system-scope cache writeback
+    and invalidation that a default event (torch.cuda.Event) performs, which
+    between back-to-back kernels costs several microseconds per record.  Used
+    for the per-step events inside the timed loop; the timed region itself
+    is bracketed by default events and synchronisations.  The HIP runtime is
+    the one libfasgd.so runs on (its symbols are looked up through the
+    library's handle)."""
+    _hip = None
+
+    def __init__(self, fa):
+        if TimingEvent._hip is None:
+            hip = fa.load_library()
+            vp = ctypes.c_void_p
+            hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(vp), ctypes.c_uint]
+            hip.hipEventRecord.argtypes = [vp, vp]
+            hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), vp, vp]
+            hip.hipEventDestroy.argtypes = [vp]
+            TimingEvent._hip = hip
+        self.handle = ctypes.c_void_p()
+        rc = TimingEvent._hip.hipEventCreateWithFlags(ctypes.byref(self.handle), HIP_EVENT_DISABLE_SYSTEM_FENCE)
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags failed ({rc})")
+
+    def __int__(self):
+        return int(self.handle.value)
+
+    def record(self):
+        import torch
+        rc = TimingEvent._hip.hipEventRecord(self.handle, ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed ({rc})")
+
+    def elapsed_time(self, end):
+        ms = ctypes.c_float()
+        rc = TimingEvent._hip.hipEventElapsedTime(ctypes.byref(ms), self.handle, end.handle)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return float(ms.value)
+
+    def __del__(self):
+        if TimingEvent._hip is not None and self.handle:
+            TimingEvent._hip.hipEventDestroy(self.handle)
+
+
 GROUPS = 5   # back-to-back groups per figure; the median of their per-call means is reported
 
 
@@ -228,7 +278,7 @@ def large_25m(fa, workload, dev, mode, K=32, reps=20):
 
     def step():
         T = st.T
-        p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        p0, p1 = TimingEvent(fa), TimingEvent(fa)
         fa.fasgd_record_next_pass(p0, p1)
         fa.fasgd_apply_with_push_and_select(st, idx, val, cnt, seg, clients[T], ts[T], pool[:K],
                                             clients[T + 1:T + 1 + K], ts[T + 1:T + 1 + K], pool[K],
@@ -470,9 +520,7 @@ def main():
 
     def step(i, timed, c):
         base = st.T                          # the schedule is indexed by server timestamp
-        p0 = torch.cuda.Event(enable_timing=True)
-        p1 = torch.cuda.Event(enable_timing=True)
-        e2 = torch.cuda.Event(enable_timing=True)
+        p0, p1, e2 = TimingEvent(fa), TimingEvent(fa), TimingEvent(fa)
         out_cnt = cnts[i + 1:i + 2]
         if pending:
             pc, pts, j = pending.pop()

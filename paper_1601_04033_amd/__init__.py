@@ -426,15 +426,18 @@ def fasgd_apply_with_push_and_select(state: State, push_idx, push_val, push_coun
 
 
 def fasgd_record_next_pass(start, stop) -> None:
-    """Record two torch.cuda.Events around the next FASGD pass kernel this
-    thread launches (diagnostics; both None clears).  The events are recorded
-    once here first, so that torch has created them."""
+    """Record two events around the next FASGD pass kernel this thread
+    launches (diagnostics; both None clears): torch.cuda.Events (recorded
+    once here first, so that torch has created them) or raw hipEvent_t
+    handles (anything int() gives the handle of)."""
     if start is None and stop is None:
         _check(load_library().fasgd_record_next_pass(None, None))
         return
-    start.record()
-    stop.record()
-    _check(load_library().fasgd_record_next_pass(int(start.cuda_event), int(stop.cuda_event)))
+    if hasattr(start, "cuda_event"):
+        start.record()
+        stop.record()
+        start, stop = start.cuda_event, stop.cuda_event
+    _check(load_library().fasgd_record_next_pass(int(start), int(stop)))
 
 
 def bfasgd_apply_sparse(state: State, idx, val, d_count, client: int, grad_ts: int, stream=None) -> None:
