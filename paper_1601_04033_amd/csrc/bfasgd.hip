@@ -621,13 +621,45 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8, 8)
         scatter_direct_tile<false, TPB, KT>(a, tile, lane, s_idx[w], s_val[w]);
 }
 
+// After a pass that took the decisions (it leaves ballot words, no counts):
+// each tile's offset within its block of TPB tiles and the blocks' 16-bit
+// totals, for select_scatter_direct.  A wave counts 64 consecutive tiles,
+// one per lane (as the scan from ballots does); a block of tiles is TPB
+// consecutive lanes, so a scan within segments of TPB lanes gives both.
 template <int TPB>
-hipError_t launch_direct(const SelectArgs& a, const SelectBatch& bt, int B, bool aligned, hipStream_t s)
+__global__ __launch_bounds__(kSelBlock) void select_count_totals(const SelectArgs a)
+{
+    static_assert(kWave % TPB == 0, "a block of tiles lies within one wave");
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * kSelBlock + threadIdx.x;
+    uint32_t c = wave_tile_bits(a, t - lane, lane);
+    if (t >= a.n_tiles) c = 0;
+    uint32_t inc = c;
+#pragma unroll
+    for (int d = 1; d < TPB; d <<= 1) {
+        const uint32_t up = __shfl_up(inc, d, kWave);
+        if (lane % TPB >= d) inc += up;
+    }
+    if (t < a.n_tiles) a.tile_offset[t] = inc - c;
+    if (lane % TPB == TPB - 1 && t - (TPB - 1) < a.n_tiles)
+        reinterpret_cast<uint16_t*>(a.group_total)[t / TPB] = static_cast<uint16_t>(inc);
+}
+
+// The two-launch selection; from_ballots (one push): the decisions were
+// taken by the preceding pass, so the first launch only counts.
+template <int TPB>
+hipError_t launch_direct(const SelectArgs& a, const SelectBatch& bt, int B, bool aligned, bool from_ballots,
+                         hipStream_t s)
 {
     const int64_t blocks = (a.n_tiles + TPB - 1) / TPB;
     const int kt = static_cast<int>((blocks + kWave * 8 - 1) / (kWave * 8));
-    const dim3 mgrid(static_cast<unsigned>(blocks), static_cast<unsigned>(B));
-    select_mark_totals<TPB><<<mgrid, TPB * kWave, 0, s>>>(a, bt, aligned);
+    if (from_ballots) {
+        select_count_totals<TPB><<<static_cast<unsigned>((a.n_tiles + kSelBlock - 1) / kSelBlock), kSelBlock, 0,
+                                   s>>>(a);
+    } else {
+        const dim3 mgrid(static_cast<unsigned>(blocks), static_cast<unsigned>(B));
+        select_mark_totals<TPB><<<mgrid, TPB * kWave, 0, s>>>(a, bt, aligned);
+    }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const dim3 grid(static_cast<unsigned>((a.n_tiles + kWavesPerBlock - 1) / kWavesPerBlock), static_cast<unsigned>(B));
@@ -731,8 +763,8 @@ hipError_t launch_select(const SelectArgs& a, const SelectBatch& bt, int B, bool
     const unsigned gx = static_cast<unsigned>((a.n_tiles + kWavesPerBlock - 1) / kWavesPerBlock);
     const unsigned groups = static_cast<unsigned>((a.n_tiles + kScanBlock - 1) / kScanBlock);
     if (groups > static_cast<unsigned>(kMaxGroups) || B < 1 || B > kMaxBatch) return hipErrorInvalidValue;
-    if (a.n_tiles <= 8 * kDirectMaxBlocks) return launch_direct<8>(a, bt, B, aligned, s);
-    if (a.n_tiles <= kDirectMaxTiles) return launch_direct<16>(a, bt, B, aligned, s);
+    if (a.n_tiles <= 8 * kDirectMaxBlocks) return launch_direct<8>(a, bt, B, aligned, false, s);
+    if (a.n_tiles <= kDirectMaxTiles) return launch_direct<16>(a, bt, B, aligned, false, s);
     hipError_t e;
     const dim3 grid(gx, static_cast<unsigned>(B));
     select_mark<<<grid, kSelBlock, 0, s>>>(a, bt, aligned);
@@ -762,6 +794,8 @@ hipError_t launch_select_after_mark(const SelectArgs& a, bool aligned, hipStream
     if (groups > static_cast<unsigned>(kMaxGroups)) return hipErrorInvalidValue;
     SelectBatch bt;
     memset(&bt, 0, sizeof bt);
+    if (a.n_tiles <= 8 * kDirectMaxBlocks) return launch_direct<8>(a, bt, 1, aligned, true, s);
+    if (a.n_tiles <= kDirectMaxTiles) return launch_direct<16>(a, bt, 1, aligned, true, s);
     hipError_t e;
     if (groups <= static_cast<unsigned>(kFusedTopGroups)) {
         select_scan<true, true><<<groups, kScanBlock, 0, s>>>(a, bt);

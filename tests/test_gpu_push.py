@@ -169,7 +169,8 @@ def _selection_buffers(P, cap, dev):
 @pytest.mark.parametrize("P,K,offset,cap_frac,base", [
     (1, 1, 0, 1.0, 0), (255, 3, 0, 1.0, 0), (257, 8, 0, 1.0, 0), (1027, 2, 0, 1.0, 4096),
     (100_003, 8, 0, 1.0, 0), (100_003, 8, 0, 0.03, 0), (262_144, 4, 0, 1.0, 0), (262_145, 4, 0, 1.0, 8),
-    (1_000_003, 33, 0, 1.0, 0), (65_537, 5, 1, 1.0, 0), (67_108_869, 2, 0, 1.0, 0)])
+    (1_000_003, 33, 0, 1.0, 0), (65_537, 5, 1, 1.0, 0), (12_000_003, 2, 0, 1.0, 0), (30_000_001, 2, 1, 0.5, 0),
+    (67_108_869, 2, 0, 1.0, 0)])
 @pytest.mark.parametrize("mode", [fa.MATH_FAST, fa.MATH_IEEE])
 def test_push_pass_and_next_selection_are_bit_identical(P, K, offset, cap_frac, base, mode):
     """fasgd_apply_with_push_and_select against fasgd_apply_with_push, then
@@ -178,8 +179,9 @@ def test_push_pass_and_next_selection_are_bit_identical(P, K, offset, cap_frac, 
     pass takes the next push's decisions itself at every size and alignment.
     Covers ragged tails (a last segment shorter than 256, a last tile whose
     later segments hold no parameter), P a multiple of 1024, a shard offset,
-    a capacity cut, arrays 4 bytes off alignment and more than 64 scan
-    groups."""
+    a capacity cut, arrays 4 bytes off alignment, the selection after the
+    pass in two launches with blocks of 8 tiles (12M) and of 16 (30M), and
+    in three launches with more than 64 scan groups (67M)."""
     import torch
     dev = gpu()
     a, b, _, (m_, s_, w), keep = _states(P, dev, mode, fa.V_EQUATIONS, seed=P % 991, offset=offset)
