@@ -21,7 +21,8 @@
 //            index order), and writes the staged run at group offset + tile
 //            offset in contiguous stores.
 // When the mark step ran inside the preceding dense pass (which leaves the
-// ballot words but no tile counts), the scan counts each tile's ballot bits.
+// ballot words but no tile counts), the scan counts each tile's ballot bits
+// (in the two-launch range, a count launch does, for the direct scatter).
 // Several pushes selected together run as one set of launches with the push
 // as the grid's y index, each with its own gradient, counter words, output
 // slice and workspace slice.
