@@ -233,6 +233,15 @@ def grouped_b2b(torch, fn, count, groups=GROUPS):
     return float(statistics.median(means)), [float(min(means)), float(max(means))]
 
 
+# Calls per back-to-back group at 25M parameters, so that every group holds
+# 5 ms or more of GPU work: the two events around a group (each a
+# system-scope cache writeback) and the first call's ramp then add well
+# under 1 % per call.  With 20 selections (0.8 ms) per group they added
+# about 0.5 us to each 38 us call.
+DENSE_25M_CALLS = {1: 40, 8: 20, 32: 10}
+SELECT_25M_CALLS = 128
+
+
 def large_25m(fa, workload, dev, mode, K=32, reps=20):
     """The 25M-parameter workload (50 blocks of 500k, lambda = 64) beside the
     main one: the dense pass at K = 1, 8, 32, the server's step (one
@@ -250,7 +259,8 @@ def large_25m(fa, workload, dev, mode, K=32, reps=20):
     theta.copy_(theta0)
     del theta0
     st = fa.fasgd_init_state(theta, n, b, v, last_T, lam=w.lam, alpha=w.alpha_fasgd, math_mode=mode)
-    clients, ts = workload.schedule(w, K + (GROUPS * 10 + 1) * (1 + 8 + 32) + (GROUPS * reps + 4) * (K + 1) + 64)
+    dense_updates = sum((GROUPS * n_calls + 1) * k for k, n_calls in DENSE_25M_CALLS.items())
+    clients, ts = workload.schedule(w, K + dense_updates + (GROUPS * reps + 4) * (K + 1) + 64)
     idx = torch.empty(P, device=dev, dtype=torch.int32)
     val = torch.empty(P, device=dev)
     cnt = torch.zeros(1, device=dev, dtype=torch.int64)
@@ -264,11 +274,11 @@ def large_25m(fa, workload, dev, mode, K=32, reps=20):
         return grouped_b2b(torch, fn, count)
 
     out = {"P": P, "lambda": w.lam, "dense": {}}
-    for k in (1, 8, 32):
+    for k, n_calls in DENSE_25M_CALLS.items():
         def dense(k=k):
             T = st.T
             fa.fasgd_apply_updates(st, pool[:k], clients[T:T + k], ts[T:T + k])
-        ms, spread = b2b(dense, 10)
+        ms, spread = b2b(dense, n_calls)
         out["dense"][f"K={k}"] = {"ms": ms, "frac": P * (32 + 4 * k) / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
                                   "ms_range": spread}
     # the server's step, its pass timed alone with events around the kernel
@@ -295,7 +305,7 @@ def large_25m(fa, workload, dev, mode, K=32, reps=20):
     T = st.T
     fa.bfasgd_apply_sparse(st, idx, val, cnt, clients[T], ts[T])
     sel_ms, sel_spread = b2b(lambda: fa.bfasgd_select_compact(st, pool[K], c, EPS_C, SEED, st.T, clients[st.T], idx,
-                                                              val, cnt, ws), reps)
+                                                              val, cnt, ws), SELECT_25M_CALLS)
     m = int(cnt.item())
     out["bfasgd_select_compact"] = {"ms": sel_ms, "frac": (8 * P + 8 * m) / (sel_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
                                     "ms_range": sel_spread}
