@@ -468,6 +468,33 @@ const char* fasgd_last_error(void);
  */
 fasgd_status fasgd_record_next_pass(hipEvent_t start, hipEvent_t stop);
 
+/*
+ * Diagnostics: checks on the device that the IEEE mode's short sequences
+ * give the correctly rounded results of the general ones, bit for bit.  In
+ * IEEE mode every update computes sqrt(x) (x = max(n - b^2, 0) + eps),
+ * 1 / sqrt(x) as two correctly rounded operations, and alpha / (v tau)
+ * (Sec. 2.2's equations for v and the rate).  When eps >= 2^-96 (finite) and
+ * 2^-20 <= |alpha| < 2^20 the kernels take shorter sequences (a hardware
+ * estimate, then corrections by exact fma residuals); this call compares them
+ * with the general sequences:
+ *   d_mismatches[0]  sqrt over every float x >= 2^-96 (+inf and NaNs too);
+ *   d_mismatches[1]  1 / sqrt(x) over the same x;
+ *   d_mismatches[2]  alpha / d over all 2^32 bit patterns of d;
+ *   d_mismatches[3]  n_updates whole updates in both readings of v, on
+ *                    pseudo-random states drawn from `seed` (zeros,
+ *                    subnormals, infinities and NaNs among them), with
+ *                    gamma, beta, eps and alpha.
+ * NaN results count as equal to NaN results.  d_mismatches: device, 4
+ * counters (8-byte aligned), cleared by the call, read after the stream is
+ * synchronised; all four are 0 when the sequences hold.  FASGD_ERR_ARG when
+ * eps or alpha lie outside the range above (the kernels use the general
+ * sequences there), gamma or beta outside [0, 1] or n_updates < 0;
+ * FASGD_ERR_NULL / FASGD_ERR_ALIGN for d_mismatches.  Takes about 10 ms of
+ * GPU time plus the updates.
+ */
+fasgd_status fasgd_check_ieee_sequences(float gamma, float beta, float eps, float alpha, uint64_t seed,
+                                        int64_t n_updates, unsigned long long* d_mismatches, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -38,7 +38,7 @@ ABI_FUNCTIONS = ("fasgd_init_state", "fasgd_apply_updates", "sasgd_apply_updates
                  "bfasgd_segments_workspace_bytes", "bfasgd_decide_segments", "bfasgd_apply_segments",
                  "bfasgd_list_index_length", "fasgd_apply_with_push",
                  "bfasgd_select_compact_batch", "fasgd_apply_pushes", "fasgd_apply_with_push_and_select",
-                 "fasgd_record_next_pass", "bfasgd_select_compact_noalloc",
+                 "fasgd_record_next_pass", "bfasgd_select_compact_noalloc", "fasgd_check_ieee_sequences",
                  "fasgd_status_string", "fasgd_last_error")
 
 # bfasgd_select_compact_noalloc: the largest P its built-in scratch holds
@@ -103,6 +103,8 @@ def load_library(path: Optional[str] = None):
                  "bfasgd_apply_segments", "fasgd_apply_with_push", "bfasgd_select_compact_noalloc"):
         getattr(lib, name).restype = ctypes.c_int
     lib.fasgd_record_next_pass.argtypes = [P, P]
+    lib.fasgd_check_ieee_sequences.argtypes = [f, f, f, f, u64, i64, P, P]
+    lib.fasgd_check_ieee_sequences.restype = ctypes.c_int
     lib.fasgd_status_string.argtypes = [ctypes.c_int]
     lib.fasgd_status_string.restype = ctypes.c_char_p
     lib.fasgd_last_error.argtypes = []
@@ -438,6 +440,21 @@ def fasgd_record_next_pass(start, stop) -> None:
         stop.record()
         start, stop = start.cuda_event, stop.cuda_event
     _check(load_library().fasgd_record_next_pass(int(start), int(stop)))
+
+
+def fasgd_check_ieee_sequences(gamma: float, beta: float, eps: float, alpha: float, seed: int, n_updates: int,
+                               mismatches, stream=None) -> None:
+    """Diagnostics: compare, on the device, the IEEE update's short correctly
+    rounded sequences with the general ones, bit for bit; the four mismatch
+    counts go to `mismatches` (int64 [4], device): square root, 1/sqrt, the
+    division alpha / d over every d, and n_updates whole updates."""
+    import torch
+    if mismatches.numel() < 4:
+        raise ValueError("mismatches needs 4 counters")
+    _check(load_library().fasgd_check_ieee_sequences(gamma, beta, eps, alpha, int(seed) & (2 ** 64 - 1),
+                                                      int(n_updates),
+                                                      _dev_ptr(mismatches, torch.int64, "mismatches"),
+                                                      _stream(stream)))
 
 
 def bfasgd_apply_sparse(state: State, idx, val, d_count, client: int, grad_ts: int, stream=None) -> None:

@@ -24,7 +24,60 @@ struct Hyper {
     float omb;     // 1 - beta
     float eps;     // inside the square root
     float alpha;   // master rate
+    int32_t rn_short;   // IEEE mode: eps >= 2^-96 and 2^-20 <= |alpha| < 2^20 (set by the host), so the
+                        // short correctly rounded sequences below hold; otherwise the general ones run
 };
+
+// Correctly rounded square root, reciprocal and division in fewer
+// instructions than the general sequences, for the operand ranges the IEEE
+// update meets once the host has checked eps and alpha.  Each starts from
+// the hardware estimate (within 1 ulp) and corrects it with exact residuals
+// computed by fused multiply-adds.  fasgd_check_ieee_sequences compares them
+// with the general sequences bit for bit, exhaustively over their ranges.
+//
+// sqrt(x), x >= 2^-96, +inf or NaN: of the estimate s and its neighbours
+// s-, s+ (one ulp away), the residuals x - s- s and x - s+ s tell on which
+// side of each midpoint the root lies (a root of a float is never exactly a
+// midpoint); at x >= 2^-96 the residuals are normal numbers, so their signs
+// are exact.
+__device__ __forceinline__ float sqrt_rn_short(float x)
+{
+    float s = __builtin_amdgcn_sqrtf(x);
+    const float sm = __int_as_float(__float_as_int(s) - 1);
+    const float sp = __int_as_float(__float_as_int(s) + 1);
+    const float rm = fmaf(-sm, s, x);
+    const float rp = fmaf(-sp, s, x);
+    s = rm <= 0.0f ? sm : s;
+    s = rp > 0.0f ? sp : s;
+    return s;
+}
+
+// 1/r for r = sqrt_rn_short(x), x >= 2^-96 (r in [2^-48, 2^64], +inf or
+// NaN): one Newton step y + y (1 - r y) with the residual exact in the fma;
+// the fix-up gives 1/inf = 0.
+__device__ __forceinline__ float rcp_of_root_rn_short(float r)
+{
+    const float y0 = __builtin_amdgcn_rcpf(r);
+    const float e = fmaf(-r, y0, 1.0f);
+    return __builtin_amdgcn_div_fixupf(fmaf(e, y0, y0), r, 1.0f);
+}
+
+// a / d for 2^-20 <= |a| < 2^20: the reciprocal as above, the quotient
+// q0 = a y, then q0 + y (a - d q0) with the remainder exact in the fma
+// (Markstein's correction).  Lanes whose |d| lies outside [2^-100, 2^100]
+// (zero, subnormal, huge, infinite or NaN divisors) take the general division.
+__device__ __forceinline__ float div_rn_short(float a, float d)
+{
+    const float y0 = __builtin_amdgcn_rcpf(d);
+    const float e = fmaf(-d, y0, 1.0f);
+    const float y = fmaf(e, y0, y0);
+    const float q0 = a * y;
+    const float r = fmaf(-d, q0, a);
+    float q = fmaf(r, y, q0);
+    const bool in_range = __builtin_fabsf(d) >= 0x1p-100f && __builtin_fabsf(d) <= 0x1p100f;
+    if (__builtin_expect(__ballot(!in_range) != 0, 0)) q = in_range ? q : a / d;
+    return q;
+}
 
 // One parameter, one gradient: the FASGD update of Sec. 2.2.
 //   n <- gamma n + (1-gamma) g^2 ; b <- gamma b + (1-gamma) g
@@ -50,6 +103,12 @@ __device__ __forceinline__ void fasgd_step(float& th, float& n, float& b, float&
         const float s = prose ? __builtin_amdgcn_sqrtf(x) : __builtin_amdgcn_rsqf(x);
         v = fmaf(h.beta, v, h.omb * s);
         th = fmaf(-(coef * __builtin_amdgcn_rcpf(v)), g, th);
+    } else if (h.rn_short) {
+        // the same correctly rounded operations as below, in the short sequences
+        const float r = sqrt_rn_short(x);
+        const float s = prose ? r : rcp_of_root_rn_short(r);
+        v = fmaf(h.beta, v, h.omb * s);
+        th = fmaf(-div_rn_short(h.alpha, v * coef), g, th);
     } else {
         const float s = prose ? sqrtf(x) : 1.0f / sqrtf(x);
         v = fmaf(h.beta, v, h.omb * s);

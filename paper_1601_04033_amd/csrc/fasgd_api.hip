@@ -93,6 +93,14 @@ int variant_of(const fasgd_state* st)
     return fasgd::kernel_variant(st->math_mode, st->v_reading == FASGD_V_PROSE);
 }
 
+// The IEEE update's short correctly rounded sequences hold for these eps and
+// alpha (x = max(n - b^2, 0) + eps >= 2^-96 under the square root; the
+// quotient alpha / (v tau) stays normal wherever the division takes them).
+bool ieee_short_ok(float eps, float alpha)
+{
+    return isfinite(eps) && eps >= 0x1p-96f && fabsf(alpha) >= 0x1p-20f && fabsf(alpha) < 0x1p20f;
+}
+
 fasgd::Hyper hyper_of(const fasgd_state* st)
 {
     fasgd::Hyper h;
@@ -102,6 +110,7 @@ fasgd::Hyper hyper_of(const fasgd_state* st)
     h.omb = 1.0f - st->beta;
     h.eps = st->eps;
     h.alpha = st->alpha;
+    h.rn_short = ieee_short_ok(st->eps, st->alpha) ? 1 : 0;
     return h;
 }
 
@@ -850,6 +859,32 @@ const char* fasgd_status_string(fasgd_status s)
 }
 
 const char* fasgd_last_error(void) { return g_err; }
+
+fasgd_status fasgd_check_ieee_sequences(float gamma, float beta, float eps, float alpha, uint64_t seed,
+                                        int64_t n_updates, unsigned long long* d_mismatches, hipStream_t stream)
+{
+    if (!d_mismatches) return fail(FASGD_ERR_NULL, "d_mismatches is NULL");
+    if (!aligned(d_mismatches, 8)) return fail(FASGD_ERR_ALIGN, "d_mismatches must be 8-byte aligned");
+    if (!(gamma >= 0.0f && gamma <= 1.0f) || !(beta >= 0.0f && beta <= 1.0f))
+        return fail(FASGD_ERR_ARG, "gamma and beta must be in [0, 1]");
+    if (!ieee_short_ok(eps, alpha))
+        return fail(FASGD_ERR_ARG,
+                    "eps = %g and alpha = %g: the short sequences need eps >= 2^-96 (finite) and "
+                    "2^-20 <= |alpha| < 2^20",
+                    static_cast<double>(eps), static_cast<double>(alpha));
+    if (n_updates < 0) return fail(FASGD_ERR_ARG, "n_updates = %lld must be >= 0", (long long)n_updates);
+    fasgd::Hyper h;
+    h.gamma = gamma;
+    h.omg = 1.0f - gamma;
+    h.beta = beta;
+    h.omb = 1.0f - beta;
+    h.eps = eps;
+    h.alpha = alpha;
+    h.rn_short = 1;
+    const hipError_t e = fasgd::launch_check_ieee(h, seed, n_updates, d_mismatches, stream);
+    if (e != hipSuccess) return hip_fail(e, "fasgd_check_ieee_sequences");
+    return ok();
+}
 
 fasgd_status fasgd_record_next_pass(hipEvent_t start, hipEvent_t stop)
 {

@@ -26,6 +26,12 @@ struct DenseArgs {
     Hyper h;
 };
 
+// Self-check of the IEEE update's short correctly rounded sequences against
+// the general ones: kIeeeChecks mismatch counters (cleared first).
+constexpr int kIeeeChecks = 4;
+hipError_t launch_check_ieee(const Hyper& h, uint64_t seed, int64_t n_updates, unsigned long long* counts,
+                             hipStream_t s);
+
 hipError_t launch_init(float* n, float* b, float* v, int32_t* last_T, int64_t P,
                        float n0, float b0, float v0, hipStream_t s);
 // variant: kernel_variant(math mode, v reading)

@@ -343,6 +343,25 @@ def test_record_next_pass_takes_both_events_or_none(lib):
     assert lib.fasgd_record_next_pass(None, None) == 0
 
 
+def test_ieee_sequence_check_rejects_bad_arguments(lib):
+    """fasgd_check_ieee_sequences accepts exactly the eps and alpha for which
+    the kernels take the short sequences (eps >= 2^-96, 2^-20 <= |alpha| <
+    2^20); every rejection happens before a launch."""
+    counts = np.zeros(5, np.int64)
+    ptr = counts.ctypes.data
+    call = lib.fasgd_check_ieee_sequences
+    assert call(0.95, 0.9, 1e-4, 0.005, 0, 16, None, None) == 1
+    assert call(0.95, 0.9, 1e-4, 0.005, 0, 16, ptr + 4, None) == 5
+    for eps, alpha in ((2.0 ** -97, 0.005), (float("inf"), 0.005), (float("nan"), 0.005), (0.0, 0.005),
+                       (1e-4, 2.0 ** -21), (1e-4, 2.0 ** 20), (1e-4, float("nan")), (1e-4, 0.0)):
+        assert call(0.95, 0.9, eps, alpha, 0, 16, ptr, None) == 2, (eps, alpha)
+    assert "2^-96" in lib.fasgd_last_error().decode()
+    assert call(1.5, 0.9, 1e-4, 0.005, 0, 16, ptr, None) == 2
+    assert call(0.95, -0.1, 1e-4, 0.005, 0, 16, ptr, None) == 2
+    assert call(0.95, 0.9, 1e-4, 0.005, 0, -1, ptr, None) == 2
+    assert (counts == 0).all()
+
+
 def test_sparse_rejects_bad_arguments(lib):
     st, f = _state(P=16, T=2)
     cnt = np.zeros(2, np.int64)

@@ -1,0 +1,59 @@
+"""GPU: the IEEE mode's short correctly rounded sequences (used when
+eps >= 2^-96 and 2^-20 <= |alpha| < 2^20) equal the general sequences bit
+for bit, checked exhaustively on the device through
+fasgd_check_ieee_sequences; and the general sequences, which run outside
+that range, still match the oracle."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1601_04033_amd as fa
+import workload
+from helpers import RTOL_SEQ, assert_state_close, gpu, new_gpu_state, to_dev
+
+pytestmark = pytest.mark.gpu
+
+# (gamma, beta, eps, alpha): the workloads' settings, the hand trace's, the
+# ends of the short range and a value drawn at random
+SETTINGS = [(0.95, 0.9, 1e-4, 0.005), (0.95, 0.9, 1e-8, 0.04), (0.5, 0.5, 9 / 16, 0.25),
+            (1.0, 0.0, 2.0 ** -96, 2.0 ** -20), (0.0, 1.0, 1.0, 2.0 ** 20 * (1 - 2.0 ** -24)),
+            (0.9, 0.99, 3e-7, 0.0123), (0.95, 0.9, 1e-4, 1000.0)]
+
+
+@pytest.mark.parametrize("gamma,beta,eps,alpha", SETTINGS)
+def test_short_sequences_equal_general_ones(gamma, beta, eps, alpha):
+    """Square root and 1/sqrt over every float x >= 2^-96, alpha / d over all
+    2^32 bit patterns of d, and 2^24 whole updates per reading of v."""
+    import torch
+    dev = gpu()
+    counts = torch.full((4,), -1, dtype=torch.int64, device=dev)
+    print(f"ieee sequences: gamma={gamma} beta={beta} eps={eps} alpha={alpha}", flush=True)
+    fa.fasgd_check_ieee_sequences(gamma, beta, eps, alpha, 0x1EEE + int(alpha * 1000), 1 << 24, counts)
+    torch.cuda.synchronize()
+    got = counts.cpu().tolist()
+    assert got == [0, 0, 0, 0], dict(zip(("sqrt", "1/sqrt", "division", "updates"), got))
+
+
+@pytest.mark.parametrize("reading", [fa.V_EQUATIONS, fa.V_PROSE])
+@pytest.mark.parametrize("eps,alpha", [(2.0 ** -100, 0.01), (1e-4, 2.0 ** -21)])
+def test_general_sequences_match_oracle(eps, alpha, reading):
+    """Outside the short sequences' range (here eps below 2^-96, or alpha
+    below 2^-20) IEEE passes take the general sequences: four K = 8 passes
+    over a ragged P against 32 oracle updates."""
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["tiny"]
+    P, K = 4099, 8
+    theta0, m, s = workload.host_params(w, P, seed=9)
+    clients, ts = workload.schedule(w, 4 * K)
+    st = new_gpu_state(theta0, dev, w.lam, alpha, fa.MATH_IEEE, eps=eps, v_reading=reading)
+    ref = oracle.init_state(theta0, alpha=alpha, eps=eps, v_reading=reading)
+    for p in range(4):
+        gs = [workload.host_gradient(w, m, s, p * K + k, seed=9) for k in range(K)]
+        sl = slice(p * K, (p + 1) * K)
+        fa.fasgd_apply_updates(st, [to_dev(g, dev) for g in gs], clients[sl], ts[sl])
+        for k, g in enumerate(gs):
+            oracle.fasgd_apply(ref, g, ts[p * K + k])
+    torch.cuda.synchronize()
+    assert np.isfinite(st.theta.cpu().numpy()).all()
+    assert_state_close(st, ref, RTOL_SEQ, what=f"eps={eps} alpha={alpha}")
