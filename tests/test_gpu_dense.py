@@ -135,22 +135,23 @@ def test_mlp_fasgd_k16_sampled(mode):
     assert_state_close(st, ref, RTOL_SEQ, js=jt, what="after 2000 updates")
 
 
-@pytest.mark.parametrize("K", [1, 8, 32])
-def test_large_25m_sampled(K):
+@pytest.mark.parametrize("K,mode", [(1, fa.MATH_FAST), (8, fa.MATH_FAST), (32, fa.MATH_FAST), (32, fa.MATH_IEEE)])
+def test_large_25m_sampled(K, mode):
     """P = 25,000,000 in 50 blocks of 500k, lambda = 64, uniform 0..2 lambda
     delays; the workload's whole sequence of 512 updates in passes of K (FAST
-    mode, the benchmarked one), checked within the whole-sequence tolerance
-    on 4096 sampled parameters after every 64 updates and at the end."""
+    mode, the benchmarked one, and IEEE mode at K = 32), checked within the
+    whole-sequence tolerance on 4096 sampled parameters after every 64
+    updates and at the end."""
     import torch
     dev = gpu()
     w = workload.WORKLOADS["large"]
     assert w.updates == 512 and w.updates % K == 0
-    print(f"large 25M: K={K}, {w.updates} updates", flush=True)
+    print(f"large 25M: K={K} mode={mode}, {w.updates} updates", flush=True)
     theta0, m, s = workload.device_params(w, dev)
     clients, ts = workload.schedule(w, w.updates)
     js = sample_indices(w.P, 4096)
     jt = torch.from_numpy(js).to(dev)
-    st = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, fa.MATH_FAST)
+    st = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, mode)
     ref = oracle.init_state(theta0[jt].cpu().numpy(), alpha=w.alpha_fasgd)
     bufs = [torch.empty(w.P, device=dev) for _ in range(K)]
     for p in range(w.updates // K):
