@@ -735,9 +735,10 @@ def main():
     sync_ms = timed(lambda: fa.sgd_sync_apply(sync_st, pool[:K], w.alpha_sasgd))
     del extra
 
-    # plain copy of one gradient buffer (4P bytes read, 4P written): the
-    # bandwidth anchor, and the known-size kernel that calibrates the
-    # rocprofv3 FETCH_SIZE / WRITE_SIZE counters
+    # plain copies of one gradient buffer (4P bytes read, 4P written): the
+    # library's streaming copy (fasgd_copy_anchor), the bandwidth anchor the
+    # pass is read against, and torch's copy, the known-size kernel that
+    # calibrates the rocprofv3 FETCH_SIZE / WRITE_SIZE counters
     anchor = torch.empty_like(pool[0])
     cp_ms = []
     for r in range(3):
@@ -748,6 +749,8 @@ def main():
         torch.cuda.synchronize()
         cp_ms.append(a.elapsed_time(b_))
     copy_gbs = 8 * P / (float(np.mean(cp_ms[1:])) * 1e-3) / 1e9
+    anchor_ms, anchor_range = grouped_b2b(torch, lambda: fa.fasgd_copy_anchor(pool[0], anchor), 4)
+    anchor_gbs = 8 * P / (anchor_ms * 1e-3) / 1e9
     del anchor
     small = small_configs(fa, workload, dev, mode)
     large = large_25m(fa, workload, dev, mode) if args.workload != "large" else None
@@ -806,7 +809,9 @@ def main():
                                        "GB/s": 4 * P / (dec1_ms * 1e-3) / 1e9},
             "bfasgd_apply_segments": {"ms_all_sent": segapply_ms,
                                       "GB/s": 40 * P / (segapply_ms * 1e-3) / 1e9},
-            "copy_anchor": {"GB/s": copy_gbs, "bytes": 8 * P},
+            "copy_anchor": {"kernel": "fasgd_copy_anchor", "GB/s": anchor_gbs, "frac": anchor_gbs / HBM_PEAK_GBS,
+                            "ms": anchor_ms, "ms_range": anchor_range, "bytes": 8 * P,
+                            "pass_vs_anchor": achieved / anchor_gbs, "torch_copy_GB/s": copy_gbs},
             "small_configs": small,
             "large_25m": large,
         },

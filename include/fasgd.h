@@ -469,6 +469,17 @@ const char* fasgd_last_error(void);
 fasgd_status fasgd_record_next_pass(hipEvent_t start, hipEvent_t stop);
 
 /*
+ * Diagnostics: the bandwidth anchor, dst[0, n) = src[0, n) by a plain
+ * streaming copy (one 16-byte vector per thread over an exact-cover grid,
+ * non-temporal loads and stores, the access pattern of the passes above).
+ * Its rate, 8 n bytes over its time, is what the machine's HBM sustains for one
+ * read and one write stream, against which the passes' rates can be read.
+ *   src, dst  device fp32 [n], 16-byte aligned, not overlapping
+ * FASGD_ERR_NULL, FASGD_ERR_ALIGN, or FASGD_ERR_ARG for n < 1 or overlap.
+ */
+fasgd_status fasgd_copy_anchor(const float* src, float* dst, int64_t n, hipStream_t stream);
+
+/*
  * Diagnostics: checks on the device that the IEEE mode's short sequences
  * give the correctly rounded results of the general ones, bit for bit.  In
  * IEEE mode every update computes sqrt(x) (x = max(n - b^2, 0) + eps),

@@ -38,7 +38,7 @@ ABI_FUNCTIONS = ("fasgd_init_state", "fasgd_apply_updates", "sasgd_apply_updates
                  "bfasgd_segments_workspace_bytes", "bfasgd_decide_segments", "bfasgd_apply_segments",
                  "bfasgd_list_index_length", "fasgd_apply_with_push",
                  "bfasgd_select_compact_batch", "fasgd_apply_pushes", "fasgd_apply_with_push_and_select",
-                 "fasgd_record_next_pass", "bfasgd_select_compact_noalloc", "fasgd_check_ieee_sequences",
+                 "fasgd_record_next_pass", "bfasgd_select_compact_noalloc", "fasgd_check_ieee_sequences", "fasgd_copy_anchor",
                  "fasgd_status_string", "fasgd_last_error")
 
 # bfasgd_select_compact_noalloc: the largest P its built-in scratch holds
@@ -104,6 +104,8 @@ def load_library(path: Optional[str] = None):
         getattr(lib, name).restype = ctypes.c_int
     lib.fasgd_record_next_pass.argtypes = [P, P]
     lib.fasgd_check_ieee_sequences.argtypes = [f, f, f, f, u64, i64, P, P]
+    lib.fasgd_copy_anchor.argtypes = [P, P, i64, P]
+    lib.fasgd_copy_anchor.restype = ctypes.c_int
     lib.fasgd_check_ieee_sequences.restype = ctypes.c_int
     lib.fasgd_status_string.argtypes = [ctypes.c_int]
     lib.fasgd_status_string.restype = ctypes.c_char_p
@@ -440,6 +442,16 @@ def fasgd_record_next_pass(start, stop) -> None:
         stop.record()
         start, stop = start.cuda_event, stop.cuda_event
     _check(load_library().fasgd_record_next_pass(int(start), int(stop)))
+
+
+def fasgd_copy_anchor(src, dst, stream=None) -> None:
+    """Diagnostics: dst[:] = src[:] by the library's plain streaming copy
+    (the bandwidth anchor); float32 tensors of one length, 16-byte aligned."""
+    import torch
+    if src.numel() != dst.numel():
+        raise ValueError("src and dst differ in length")
+    _check(load_library().fasgd_copy_anchor(_dev_ptr(src, torch.float32, "src"), _dev_ptr(dst, torch.float32, "dst"),
+                                            src.numel(), _stream(stream)))
 
 
 def fasgd_check_ieee_sequences(gamma: float, beta: float, eps: float, alpha: float, seed: int, n_updates: int,

@@ -9,7 +9,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libfasgd.so")
-SOURCES = ["fasgd_api.hip", "dense.hip", "bfasgd.hip", "segments.hip", "pushes.hip", "selfcheck.hip"]
+SOURCES = ["fasgd_api.hip", "dense.hip", "bfasgd.hip", "segments.hip", "pushes.hip", "selfcheck.hip", "anchor.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

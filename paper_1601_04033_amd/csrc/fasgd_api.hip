@@ -8,6 +8,7 @@
 #include <mutex>
 
 #include "../../include/fasgd.h"
+#include "anchor.hpp"
 #include "kernels.hpp"
 
 static_assert(FASGD_MAX_K == fasgd::kMaxK, "K limit mismatch");
@@ -859,6 +860,21 @@ const char* fasgd_status_string(fasgd_status s)
 }
 
 const char* fasgd_last_error(void) { return g_err; }
+
+fasgd_status fasgd_copy_anchor(const float* src, float* dst, int64_t n, hipStream_t stream)
+{
+    if (!src || !dst) return fail(FASGD_ERR_NULL, "src or dst is NULL");
+    if (n < 1) return fail(FASGD_ERR_ARG, "n = %lld must be >= 1", (long long)n);
+    if ((n + 3) / 4 + 1 > int64_t(0xffffffff) * 256)
+        return fail(FASGD_ERR_ARG, "n = %lld is beyond one launch", (long long)n);
+    if (!aligned(src, 16) || !aligned(dst, 16)) return fail(FASGD_ERR_ALIGN, "src and dst must be 16-byte aligned");
+    const char* s = static_cast<const char*>(static_cast<const void*>(src));
+    const char* d = static_cast<const char*>(static_cast<const void*>(dst));
+    if (s < d + 4 * n && d < s + 4 * n) return fail(FASGD_ERR_ARG, "src and dst overlap");
+    const hipError_t e = fasgd::launch_copy_anchor(src, dst, n, stream);
+    if (e != hipSuccess) return hip_fail(e, "fasgd_copy_anchor");
+    return ok();
+}
 
 fasgd_status fasgd_check_ieee_sequences(float gamma, float beta, float eps, float alpha, uint64_t seed,
                                         int64_t n_updates, unsigned long long* d_mismatches, hipStream_t stream)

@@ -362,6 +362,19 @@ def test_ieee_sequence_check_rejects_bad_arguments(lib):
     assert (counts == 0).all()
 
 
+def test_copy_anchor_rejects_bad_arguments(lib):
+    buf = np.zeros(64, np.float32)
+    base = buf.ctypes.data
+    a = base + (-base) % 16                      # a 16-byte aligned address inside buf
+    assert lib.fasgd_copy_anchor(None, a, 4, None) == 1
+    assert lib.fasgd_copy_anchor(a, None, 4, None) == 1
+    assert lib.fasgd_copy_anchor(a, a + 64, 0, None) == 2
+    assert lib.fasgd_copy_anchor(a + 4, a + 64, 4, None) == 5
+    assert lib.fasgd_copy_anchor(a, a + 68, 4, None) == 5
+    assert lib.fasgd_copy_anchor(a, a + 16, 8, None) == 2        # overlapping ranges
+    assert "overlap" in lib.fasgd_last_error().decode()
+
+
 def test_sparse_rejects_bad_arguments(lib):
     st, f = _state(P=16, T=2)
     cnt = np.zeros(2, np.int64)

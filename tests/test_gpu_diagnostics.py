@@ -1,8 +1,9 @@
-"""GPU: the IEEE mode's short correctly rounded sequences (used when
-eps >= 2^-96 and 2^-20 <= |alpha| < 2^20) equal the general sequences bit
-for bit, checked exhaustively on the device through
-fasgd_check_ieee_sequences; and the general sequences, which run outside
-that range, still match the oracle."""
+"""GPU: the diagnostics entry points.  The IEEE mode's short correctly
+rounded sequences (used when eps >= 2^-96 and 2^-20 <= |alpha| < 2^20)
+equal the general sequences bit for bit, checked exhaustively on the device
+through fasgd_check_ieee_sequences; the general sequences, which run outside
+that range, still match the oracle; and the bandwidth anchor copies
+exactly."""
 import numpy as np
 import pytest
 
@@ -57,3 +58,17 @@ def test_general_sequences_match_oracle(eps, alpha, reading):
     torch.cuda.synchronize()
     assert np.isfinite(st.theta.cpu().numpy()).all()
     assert_state_close(st, ref, RTOL_SEQ, what=f"eps={eps} alpha={alpha}")
+
+
+@pytest.mark.parametrize("n", [1, 3, 4, 5, 1023, 1 << 20, (1 << 22) + 7])
+def test_copy_anchor_copies_exactly(n):
+    """The bandwidth anchor (fasgd_copy_anchor) copies every float bit for bit,
+    the trailing n % 4 included, and writes nothing past n."""
+    import torch
+    dev = gpu()
+    src = torch.randn(n, device=dev)
+    dst = torch.full((n + 4,), 7.0, device=dev)
+    fa.fasgd_copy_anchor(src, dst[:n])
+    torch.cuda.synchronize()
+    assert torch.equal(dst[:n].view(torch.int32), src.view(torch.int32))
+    assert (dst[n:] == 7.0).all()
