@@ -73,7 +73,11 @@ def _calibrate_c(v, target):
     return oracle.f32(c)
 
 
-def test_memscale_1e9_step_sampled():
+@pytest.mark.parametrize("mode", [fa.MATH_FAST, fa.MATH_IEEE])
+def test_memscale_1e9_step_sampled(mode):
+    """1e9 parameters: a K = 32 pass, then a B-FASGD push selected at about
+    10 % and applied sparsely, in FAST math (the benchmarked mode) and in
+    IEEE math; the state on 4096 sampled parameters against the oracle."""
     import torch
     dev = gpu()
     w = workload.WORKLOADS["memscale"]
@@ -81,12 +85,12 @@ def test_memscale_1e9_step_sampled():
     free, total = torch.cuda.mem_get_info()
     if free < 170e9:
         pytest.skip(f"needs about 170 GB of free device memory, {free / 1e9:.0f} GB free")
-    print(f"memscale: P={P} K={K}", flush=True)
+    print(f"memscale: P={P} K={K} mode={mode}", flush=True)
     theta0, m, s = workload.device_params(w, dev)
     clients, ts = workload.schedule(w, K + 1)
     js = sample_indices(P, 4096, seed=1)
     jt = torch.from_numpy(js).to(dev)
-    st = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, fa.MATH_FAST)
+    st = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, mode)
     ref = oracle.init_state(theta0[jt].cpu().numpy(), alpha=w.alpha_fasgd)
     del theta0
     grads = [workload.device_gradient(w, m, s, t) for t in range(K + 1)]
