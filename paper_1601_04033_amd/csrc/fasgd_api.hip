@@ -868,9 +868,9 @@ fasgd_status fasgd_copy_anchor(const float* src, float* dst, int64_t n, hipStrea
     if ((n + 3) / 4 + 1 > int64_t(0xffffffff) * 256)
         return fail(FASGD_ERR_ARG, "n = %lld is beyond one launch", (long long)n);
     if (!aligned(src, 16) || !aligned(dst, 16)) return fail(FASGD_ERR_ALIGN, "src and dst must be 16-byte aligned");
-    const char* s = static_cast<const char*>(static_cast<const void*>(src));
-    const char* d = static_cast<const char*>(static_cast<const void*>(dst));
-    if (s < d + 4 * n && d < s + 4 * n) return fail(FASGD_ERR_ARG, "src and dst overlap");
+    const uintptr_t s = reinterpret_cast<uintptr_t>(src), d = reinterpret_cast<uintptr_t>(dst);
+    const uintptr_t len = static_cast<uintptr_t>(n) * sizeof(float);
+    if (s < d + len && d < s + len) return fail(FASGD_ERR_ARG, "src and dst overlap");
     const hipError_t e = fasgd::launch_copy_anchor(src, dst, n, stream);
     if (e != hipSuccess) return hip_fail(e, "fasgd_copy_anchor");
     return ok();
