@@ -72,3 +72,33 @@ def test_copy_anchor_copies_exactly(n):
     torch.cuda.synchronize()
     assert torch.equal(dst[:n].view(torch.int32), src.view(torch.int32))
     assert (dst[n:] == 7.0).all()
+
+
+def test_ieee_division_fallback_inside_the_pass():
+    """Inside the K-fused IEEE pass, lanes whose divisor v tau lies outside
+    [2^-100, 2^100] take the general division while the other lanes of the
+    same wave take the short one: v starts at 1e-33, 1e33 or 1 in turn and
+    beta = 1 keeps it there, so every wave mixes the two.  Positive gradients
+    keep theta's sums free of cancellation.  Two K = 8 passes over a ragged P
+    against 16 oracle updates."""
+    import torch
+    dev = gpu()
+    w = workload.WORKLOADS["tiny"]
+    P, K = 4099, 8
+    theta0, m, s = workload.host_params(w, P, seed=11)
+    clients, ts = workload.schedule(w, 2 * K)
+    v0 = np.where(np.arange(P) % 3 == 0, 1e-33, np.where(np.arange(P) % 3 == 1, 1e33, 1.0)).astype(np.float32)
+    st = new_gpu_state(theta0, dev, w.lam, w.alpha_fasgd, fa.MATH_IEEE, beta=1.0)
+    st.v.copy_(torch.from_numpy(v0))
+    ref = oracle.init_state(theta0, alpha=w.alpha_fasgd, beta=1.0)
+    ref.v = v0.astype(np.float64)
+    for p in range(2):
+        gs = [np.abs(workload.host_gradient(w, m, s, p * K + k, seed=11)) + np.float32(1e-3) for k in range(K)]
+        sl = slice(p * K, (p + 1) * K)
+        fa.fasgd_apply_updates(st, [to_dev(g, dev) for g in gs], clients[sl], ts[sl])
+        for k, g in enumerate(gs):
+            oracle.fasgd_apply(ref, g, ts[p * K + k])
+    torch.cuda.synchronize()
+    th = st.theta.cpu().numpy()
+    assert np.isfinite(th).all() and (np.abs(th[0::3]) > 1e25).all()    # the tiny divisors took effect
+    assert_state_close(st, ref, RTOL_SEQ, what="mixed divisor ranges")
